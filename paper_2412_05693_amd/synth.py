@@ -1,0 +1,233 @@
+"""Seeded synthetic workloads for P&D KV-compressed attention.
+
+This module only draws inputs; it holds none of the method's arithmetic, and it
+is the one piece that both the HIP path's harness and the CPU oracle's tests
+use.  It never imports the oracle or the native library.
+
+Recipe (stand-in for the long-input, short-output tasks of Sec. 4 -- CNN/DM,
+NarrativeQA, GSM8K -- whose data and model weights are not used here):
+
+* Q, K, V elements are N(0, 1) / sqrt(d), drawn in float64 by numpy's PCG64 and
+  rounded once to float32.
+* Heavy hitters: a share of the *prompt* key positions has its K rows scaled
+  (x4) in float32; "sink" positions 0..3 are scaled x6.  Decode-step inputs
+  are never scaled.  The positions are shared by every KV head of a sample.
+* bf16 workloads round the float32 values to bf16 (round to nearest even)
+  once, on the host; both sides then see exactly those values.
+
+Per-unit streams: the unit (layer, sample, kv_head) draws, in this order,
+K[s+D, d], V[s+D, d], Q[G, s+D, d] from
+``PCG64(SeedSequence([seed, 0, layer, sample, kv_head]))``; heavy-hitter
+positions come from ``SeedSequence([seed, 1, layer, sample])``.  Bulk units of
+large configurations are drawn on the device with ``torch.randn`` (timing
+only, same distributions and the same heavy-hitter positions); checked units
+are overwritten with the host stream so the oracle can reproduce them.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str            # "f32" or "bf16"
+    b: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    s: int                # prompt length
+    kv_max: int           # cache bound |kv|-bar
+    block: int            # prefill block (the paper's p)
+    n_decode: int         # decode steps
+    hh_mode: str          # "scatter", "spans" or "none"
+    hh_frac: float = 0.02
+    hh_scale: float = 4.0
+    n_sinks: int = 0
+    sink_scale: float = 6.0
+    n_spans: int = 8
+    span_len: int = 64
+    n_layers: int = 1
+    seed: int = 1
+
+    @property
+    def group(self) -> int:
+        return self.n_heads // self.n_kv_heads
+
+    @property
+    def units(self) -> int:
+        return self.b * self.n_kv_heads
+
+    @property
+    def total(self) -> int:
+        return self.s + self.n_decode
+
+    @property
+    def sm_scale(self) -> float:
+        return 1.0 / float(np.sqrt(self.head_dim))
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+# The five workloads of the benchmark suite.  c4's prefill block is not given
+# by the workload statement; 256 (as in c2 and c5) is used.
+WORKLOADS = {
+    "c1": Workload("c1-fp32-mha-b2-s512", "f32", b=2, n_heads=4, n_kv_heads=4, head_dim=64,
+                   s=512, kv_max=128, block=64, n_decode=32, hh_mode="scatter", seed=1),
+    "c2": Workload("c2-llama3-8b-layer-b64-s4096", "bf16", b=64, n_heads=32, n_kv_heads=8,
+                   head_dim=128, s=4096, kv_max=512, block=256, n_decode=128,
+                   hh_mode="scatter", n_sinks=4, seed=2),
+    "c3": Workload("c3-long-prefill-b128-s16384", "bf16", b=128, n_heads=32, n_kv_heads=8,
+                   head_dim=128, s=16384, kv_max=1024, block=512, n_decode=64,
+                   hh_mode="spans", n_sinks=4, seed=3),
+    "c4": Workload("c4-decode-heavy-b1024-s2048", "bf16", b=1024, n_heads=32, n_kv_heads=8,
+                   head_dim=128, s=2048, kv_max=512, block=256, n_decode=512,
+                   hh_mode="scatter", n_sinks=4, seed=4),
+    "c5": Workload("c5-llama3-8b-32layer-s8192", "bf16", b=0, n_heads=32, n_kv_heads=8,
+                   head_dim=128, s=8192, kv_max=512, block=256, n_decode=256,
+                   hh_mode="scatter", n_sinks=4, n_layers=32, seed=5),
+}
+
+# A supplementary "sharp" distribution: Q, K ~ N(0, 1) per element (no 1/sqrt(d)),
+# which spreads the averages apart so kept-set comparisons are discriminating.
+SHARP_SEED = 101
+
+
+# ---------------------------------------------------------------------------
+# bf16 helpers (input preparation only)
+# ---------------------------------------------------------------------------
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (nearest, ties to even); return uint16 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def round_to_dtype(x: np.ndarray, dtype: str) -> np.ndarray:
+    """float32 values exactly representable in the workload's element type."""
+    x = np.asarray(x, dtype=np.float32)
+    if dtype == "f32":
+        return x
+    if dtype == "bf16":
+        return bf16_bits_to_f32(f32_to_bf16_bits(x))
+    raise ValueError(dtype)
+
+
+# ---------------------------------------------------------------------------
+# heavy hitters and sinks
+# ---------------------------------------------------------------------------
+def heavy_positions(wl: Workload, layer: int, sample: int) -> np.ndarray:
+    """Prompt positions whose keys are scaled by ``hh_scale`` (sorted, unique)."""
+    if wl.hh_mode == "none":
+        return np.zeros(0, dtype=np.int64)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([wl.seed, 1, layer, sample])))
+    lo = wl.n_sinks
+    if wl.hh_mode == "scatter":
+        count = int(round(wl.hh_frac * wl.s))
+        pos = rng.choice(np.arange(lo, wl.s), size=count, replace=False)
+        return np.sort(pos).astype(np.int64)
+    if wl.hh_mode == "spans":
+        # n_spans non-overlapping spans: one random span per equal segment of [lo, s)
+        seg = (wl.s - lo) // wl.n_spans
+        if seg < wl.span_len:
+            raise ValueError("prompt too short for the requested spans")
+        out = []
+        for i in range(wl.n_spans):
+            start = lo + i * seg + int(rng.integers(0, seg - wl.span_len + 1))
+            out.append(np.arange(start, start + wl.span_len))
+        return np.concatenate(out).astype(np.int64)
+    raise ValueError(wl.hh_mode)
+
+
+def key_scale_profile(wl: Workload, layer: int, sample: int) -> np.ndarray:
+    """Per-position multiplier of K rows: 1, hh_scale or sink_scale ([s + D])."""
+    prof = np.ones(wl.total, dtype=np.float32)
+    prof[heavy_positions(wl, layer, sample)] = np.float32(wl.hh_scale)
+    prof[: wl.n_sinks] = np.float32(wl.sink_scale)
+    return prof
+
+
+# ---------------------------------------------------------------------------
+# per-unit host streams (checked units)
+# ---------------------------------------------------------------------------
+def unit_inputs(wl: Workload, layer: int, sample: int, kv_head: int, sharp: bool = False):
+    """Inputs of one unit as float32 arrays exactly representable in wl.dtype.
+
+    Returns q [G, s+D, d], k [s+D, d], v [s+D, d].
+    """
+    d, T, G = wl.head_dim, wl.total, wl.group
+    seed = SHARP_SEED if sharp else wl.seed
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0, layer, sample, kv_head])))
+    k = rng.standard_normal((T, d))
+    v = rng.standard_normal((T, d))
+    q = rng.standard_normal((G, T, d))
+    scale = 1.0 / np.sqrt(d)
+    v = (v * scale).astype(np.float32)
+    if sharp:
+        k = k.astype(np.float32)
+        q = q.astype(np.float32)
+    else:
+        k = (k * scale).astype(np.float32)
+        q = (q * scale).astype(np.float32)
+        k = k * key_scale_profile(wl, layer, sample)[:, None]
+    return (round_to_dtype(q, wl.dtype), round_to_dtype(k, wl.dtype), round_to_dtype(v, wl.dtype))
+
+
+def checked_units(wl: Workload, count: int, seed: int = 0) -> list:
+    """A seeded sample of (sample, kv_head) units that always holds the first and
+    the last unit; all units when ``count`` covers them."""
+    U = wl.units
+    if count >= U:
+        return [(u // wl.n_kv_heads, u % wl.n_kv_heads) for u in range(U)]
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([wl.seed, 2, seed])))
+    pick = set([0, U - 1])
+    rest = rng.choice(np.arange(1, U - 1), size=count - 2, replace=False)
+    pick.update(int(x) for x in rest)
+    return [(u // wl.n_kv_heads, u % wl.n_kv_heads) for u in sorted(pick)]
+
+
+# ---------------------------------------------------------------------------
+# full-batch tensors (torch; device or CPU)
+# ---------------------------------------------------------------------------
+def batch_inputs(wl: Workload, device, layer: int = 0, checked=(), sharp: bool = False,
+                 gen_seed: int | None = None):
+    """q [b, H, s+D, d], k/v [b, Hk, s+D, d] in the workload's dtype.
+
+    Bulk values come from ``torch.randn`` under a seeded generator on
+    ``device``; units listed in ``checked`` (pairs (sample, kv_head)) are
+    overwritten with their host stream (``unit_inputs``).
+    """
+    import torch
+
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    b, H, Hk, d, T, G = wl.b, wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.total, wl.group
+    g = torch.Generator(device=device)
+    g.manual_seed((gen_seed if gen_seed is not None else wl.seed) * 1000003 + layer)
+    scale = 1.0 if sharp else 1.0 / float(np.sqrt(d))
+
+    def draw(shape, s):
+        x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        if s != 1.0:
+            x.mul_(s)
+        return x
+
+    k = draw((b, Hk, T, d), scale)
+    if not sharp:
+        prof = np.stack([key_scale_profile(wl, layer, i) for i in range(b)])     # [b, T]
+        k.mul_(torch.from_numpy(prof).to(device)[:, None, :, None])
+    k = k.to(tdt)
+    v = draw((b, Hk, T, d), 1.0 / float(np.sqrt(d))).to(tdt)
+    q = draw((b, H, T, d), scale).to(tdt)
+    for (bi, hk) in checked:
+        uq, uk, uv = unit_inputs(wl, layer, bi, hk, sharp=sharp)
+        q[bi, hk * G:(hk + 1) * G] = torch.from_numpy(uq).to(device=device, dtype=tdt)
+        k[bi, hk] = torch.from_numpy(uk).to(device=device, dtype=tdt)
+        v[bi, hk] = torch.from_numpy(uv).to(device=device, dtype=tdt)
+    return q, k, v

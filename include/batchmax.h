@@ -1,0 +1,176 @@
+/*
+ * batchmax.h -- C ABI of the MI355X (gfx950) Batch-Max P&D attention library.
+ *
+ * Batch-Max (arXiv 2412.05693) bounds the KV cache of every attention head of
+ * every sample to |kv|-bar pairs during both prefill and decode (Sec. 3).
+ * Prefill runs block by block (Sec. 3.1, Algorithm 1); each block's queries
+ * attend causally to the bounded cache plus the block's own keys; every key
+ * accumulates the attention probabilities it receives (sum_weights, Sec. 3.2);
+ * the cache is then cut back to |kv|-bar by removing the entries with the
+ * smallest average attention sum_weights / (curr_id + 1 - kv_ids) (Sec. 3.2),
+ * the older entry first on an exact tie, and the survivors are compacted in
+ * place.  Decode repeats this with one query position and one removal per step.
+ *
+ * Terms.  A *unit* is one (sample, KV head) pair; with grouped-query attention
+ * its G = n_heads / n_kv_heads query heads share its cache and their
+ * probabilities are summed into its scores.  Query head h reads KV head
+ * h / G.  cap = kv_max + block slots are allocated per unit.
+ *
+ * Ownership.  The caller owns every device buffer (for example torch tensors)
+ * and keeps them alive until the enqueued work has finished.  The library
+ * never allocates or frees device memory and never synchronises a stream; all
+ * device work is enqueued on the stream passed to each call.  bm_ctx is a small
+ * host object (dimensions, borrowed pointers, the host copy of the cache length
+ * and of the next position) created by bm_init or bm_resume and freed by
+ * bm_destroy.  A context is not thread-safe; separate contexts are independent.
+ *
+ * Errors.  Every call returns a bm_status.  Argument, capacity and order checks
+ * run on the host before anything is enqueued; on such an error the context
+ * and the cache are untouched and bm_last_error() describes the problem.  A
+ * failed kernel launch returns BM_ERR_HIP.  Faults inside kernels surface at
+ * the caller's next synchronisation of the stream.  No C++ exception crosses
+ * this boundary.
+ *
+ * Element types.  BM_F32: q, k, v, o and the K/V cache are float32.  BM_BF16:
+ * they are bfloat16 with float32 accumulation.  Scores are always float32 and
+ * positions int32.
+ */
+#ifndef BATCHMAX_H
+#define BATCHMAX_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BM_ABI_VERSION 1
+
+typedef enum bm_status {
+  BM_OK = 0,
+  BM_ERR_INVALID_ARG = 1,  /* null pointer, non-positive size, bad divisibility  */
+  BM_ERR_UNSUPPORTED = 2,  /* head_dim, dtype or group size this build lacks     */
+  BM_ERR_CAPACITY = 3,     /* the call would overflow the cap = kv_max+block slots */
+  BM_ERR_ORDER = 4,        /* position or phase out of the schedule's order      */
+  BM_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed          */
+} bm_status;
+
+typedef enum bm_dtype { BM_F32 = 0, BM_BF16 = 1 } bm_dtype;
+
+/* Problem statement (Sec. 3 and Algorithm 1): batch b, padded prompt length
+ * s (s-bar), cache bound kv_max (|kv|-bar), prefill block (the removal amount
+ * p of Algorithm 1), decode steps max_gen, and the attention shape.
+ * Supported: head_dim 64 or 128; group n_heads / n_kv_heads of 1, 2 or 4;
+ * 1 <= block <= 1024; kv_max >= 1; kv_max + block <= 4096. */
+typedef struct bm_dims {
+  int32_t b;
+  int32_t s;
+  int32_t kv_max;
+  int32_t block;
+  int32_t max_gen;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t dtype;     /* bm_dtype */
+  float sm_scale;    /* softmax scale of q.k; 0 selects 1/sqrt(head_dim) */
+} bm_dims;
+
+/* The bounded cache, caller-owned device memory, all C-contiguous.
+ *   k, v   [b, n_kv_heads, cap, head_dim]  element type of dims.dtype
+ *   score  [b, n_kv_heads, cap]  float32   sum_weights of every entry
+ *   pos    [b, n_kv_heads, cap]  int32     kv_ids (token position) of every entry
+ *   len    [b, n_kv_heads]       int32     |kv|: entries 0..len-1 are live
+ *   work   bm_workspace_bytes(dims) bytes of scratch (partial score sums,
+ *          eviction lists); contents need not survive between calls.
+ * Slot order inside a unit carries no meaning: every result depends only on
+ * the set of live entries (Sec. 3.2 treats them as a set of position ids). */
+typedef struct bm_cache {
+  void* k;
+  void* v;
+  float* score;
+  int32_t* pos;
+  int32_t* len;
+  void* work;
+  size_t work_bytes;
+} bm_cache;
+
+typedef struct bm_ctx bm_ctx;
+
+/* BM_ABI_VERSION of the loaded library. */
+int bm_abi_version(void);
+
+/* Text of the last non-OK status returned on this thread ("" if none). */
+const char* bm_last_error(void);
+
+/* cap = kv_max + block slots per unit; -1 if dims are invalid. */
+int32_t bm_cache_slots(const bm_dims* dims);
+
+/* Bytes of bm_cache.work the calls need; 0 if dims are invalid. */
+size_t bm_workspace_bytes(const bm_dims* dims);
+
+/* Check dims alone (no device work).  BM_OK, BM_ERR_INVALID_ARG or
+ * BM_ERR_UNSUPPORTED. */
+int bm_validate_dims(const bm_dims* dims);
+
+/* Start a new P&D run over `cache` (Algorithm 1 starts from an empty cache):
+ * validates dims and pointers, creates the host context, and enqueues on
+ * `stream` the zeroing of len and score.  Next expected prefill position: 0. */
+int bm_init(const bm_dims* dims, const bm_cache* cache, hipStream_t stream, bm_ctx** out);
+
+/* Create a context over a cache that already holds a valid state (for
+ * example one restored from a snapshot): `len` live entries per unit (the same
+ * for every unit) and `next_pos` the next position to process.  No device
+ * work.  Phase: prefill while next_pos < s, decode afterwards. */
+int bm_resume(const bm_dims* dims, const bm_cache* cache, int32_t len, int32_t next_pos,
+              bm_ctx** out);
+
+/* Prefill one block (Algorithm 1, processing step, Sec. 3.1; score update of
+ * Sec. 3.2): the n_tok prompt tokens at positions t0 .. t0+n_tok-1 are
+ * appended to every unit's cache (score 0, pos = position) and each of their
+ * queries attends causally to the live entries plus the block's keys up to
+ * its own position; outputs go to o and every entry's score grows by the
+ * probabilities it received from all G query heads of the unit.  No removal.
+ *   q, o  point at row t0 of [b, n_heads, seq_ld, head_dim] buffers
+ *   k, v  point at row t0 of [b, n_kv_heads, seq_ld, head_dim] buffers
+ *   seq_ld >= n_tok: rows between consecutive (sample, head) planes.
+ * Order: t0 must equal the next expected position, 1 <= n_tok <= block,
+ * t0 + n_tok <= s, and the cache must hold at most kv_max entries (evict first). */
+int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q, const void* k,
+                     const void* v, void* o, int32_t seq_ld, hipStream_t stream);
+
+/* Cut every unit back to kv_max entries (Algorithm 1 removal step; rule of
+ * Sec. 3.2): rank entries by ave = score / (curr_id + 1 - pos) ascending, then
+ * by pos ascending, remove the first len - kv_max, and fill the holes among
+ * slots 0..kv_max-1 with the survivors from slots kv_max..len-1 (K row, V row,
+ * score, pos).  curr_id must be the last processed position.  No-op when the
+ * cache holds at most kv_max entries. */
+int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream);
+
+/* One decode step at position `pos` (Algorithm 1 decode loop with one removal
+ * per step): append the step's (k, v), let the G queries attend to all live
+ * entries and the new one, add their probabilities to the scores, and, if the
+ * cache then holds more than kv_max entries, remove the one with the smallest
+ * (ave, pos) with curr_id = pos -- in place: the new entry overwrites the
+ * removed slot, or is dropped if it is itself the one removed.
+ *   q, o  point at [b, n_heads, seq_ld, head_dim] row 0 (the step's row)
+ *   k, v  point at [b, n_kv_heads, seq_ld, head_dim] row 0
+ * Order: prefill finished (pos == s on the first step, then consecutive),
+ * pos < s + max_gen, and the cache holds at most kv_max entries. */
+int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void* k, const void* v,
+                   void* o, int32_t seq_ld, hipStream_t stream);
+
+/* Host copies of the uniform cache length and of the next expected position
+ * (-1 for a null context). */
+int32_t bm_ctx_len(const bm_ctx* ctx);
+int32_t bm_ctx_next_pos(const bm_ctx* ctx);
+
+/* Free the host context (the cache is not touched). */
+void bm_destroy(bm_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BATCHMAX_H */

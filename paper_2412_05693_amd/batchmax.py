@@ -1,0 +1,317 @@
+"""Thin ctypes binding of ``libbatchmax.so`` (include/batchmax.h).
+
+The functions named ``bm_*`` mirror the C ABI one to one: they marshal
+arguments (integers, pointers as Python ints, ctypes structs) and raise
+``BatchMaxError`` on a non-OK status.  Every step of the path runs in the HIP
+kernels behind the library; nothing here computes.
+
+``PDAttention`` is a convenience owner of the cache tensors (torch allocates the
+device memory; the library never does) that checks dtype, device, shape and
+contiguity before handing raw pointers and the current HIP stream to the ABI.
+
+Importing this module loads the library and fails loudly if it is missing:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libbatchmax.so")
+
+BM_OK, BM_ERR_INVALID_ARG, BM_ERR_UNSUPPORTED, BM_ERR_CAPACITY, BM_ERR_ORDER, BM_ERR_HIP = range(6)
+BM_F32, BM_BF16 = 0, 1
+STATUS_NAMES = {0: "BM_OK", 1: "BM_ERR_INVALID_ARG", 2: "BM_ERR_UNSUPPORTED",
+                3: "BM_ERR_CAPACITY", 4: "BM_ERR_ORDER", 5: "BM_ERR_HIP"}
+
+
+class BatchMaxError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class bm_dims(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int32), ("s", ctypes.c_int32), ("kv_max", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("max_gen", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("sm_scale", ctypes.c_float)]
+
+
+class bm_cache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("score", ctypes.c_void_p),
+                ("pos", ctypes.c_void_p), ("len", ctypes.c_void_p), ("work", ctypes.c_void_p),
+                ("work_bytes", ctypes.c_size_t)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2412_05693_amd.build` "
+            "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    dims_p, cache_p = ctypes.POINTER(bm_dims), ctypes.POINTER(bm_cache)
+    sig = {
+        "bm_abi_version": (ctypes.c_int, []),
+        "bm_last_error": (ctypes.c_char_p, []),
+        "bm_cache_slots": (I32, [dims_p]),
+        "bm_workspace_bytes": (SZ, [dims_p]),
+        "bm_validate_dims": (ctypes.c_int, [dims_p]),
+        "bm_init": (ctypes.c_int, [dims_p, cache_p, P, ctypes.POINTER(P)]),
+        "bm_resume": (ctypes.c_int, [dims_p, cache_p, I32, I32, ctypes.POINTER(P)]),
+        "bm_prefill_block": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
+        "bm_evict_compact": (ctypes.c_int, [P, I32, P]),
+        "bm_decode_step": (ctypes.c_int, [P, I32, P, P, P, P, I32, P]),
+        "bm_ctx_len": (I32, [P]),
+        "bm_ctx_next_pos": (I32, [P]),
+        "bm_destroy": (None, [P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
+            "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block", "bm_evict_compact",
+            "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy")
+
+
+def _check(status: int) -> None:
+    if status != BM_OK:
+        raise BatchMaxError(status, _lib.bm_last_error().decode())
+
+
+# ---------------------------------------------------------------------------
+# one-to-one ABI wrappers
+# ---------------------------------------------------------------------------
+def bm_abi_version() -> int:
+    return _lib.bm_abi_version()
+
+
+def bm_last_error() -> str:
+    return _lib.bm_last_error().decode()
+
+
+def bm_cache_slots(dims: bm_dims) -> int:
+    return _lib.bm_cache_slots(ctypes.byref(dims))
+
+
+def bm_workspace_bytes(dims: bm_dims) -> int:
+    return _lib.bm_workspace_bytes(ctypes.byref(dims))
+
+
+def bm_validate_dims(dims: bm_dims) -> None:
+    _check(_lib.bm_validate_dims(ctypes.byref(dims)))
+
+
+def bm_init(dims: bm_dims, cache: bm_cache, stream: int) -> int:
+    out = ctypes.c_void_p()
+    _check(_lib.bm_init(ctypes.byref(dims), ctypes.byref(cache), stream, ctypes.byref(out)))
+    return out.value
+
+
+def bm_resume(dims: bm_dims, cache: bm_cache, length: int, next_pos: int) -> int:
+    out = ctypes.c_void_p()
+    _check(_lib.bm_resume(ctypes.byref(dims), ctypes.byref(cache), length, next_pos,
+                          ctypes.byref(out)))
+    return out.value
+
+
+def bm_prefill_block(ctx: int, t0: int, n_tok: int, q: int, k: int, v: int, o: int,
+                     seq_ld: int, stream: int) -> None:
+    _check(_lib.bm_prefill_block(ctx, t0, n_tok, q, k, v, o, seq_ld, stream))
+
+
+def bm_evict_compact(ctx: int, curr_id: int, stream: int) -> None:
+    _check(_lib.bm_evict_compact(ctx, curr_id, stream))
+
+
+def bm_decode_step(ctx: int, pos: int, q: int, k: int, v: int, o: int, seq_ld: int,
+                   stream: int) -> None:
+    _check(_lib.bm_decode_step(ctx, pos, q, k, v, o, seq_ld, stream))
+
+
+def bm_ctx_len(ctx: int) -> int:
+    return _lib.bm_ctx_len(ctx)
+
+
+def bm_ctx_next_pos(ctx: int) -> int:
+    return _lib.bm_ctx_next_pos(ctx)
+
+
+def bm_destroy(ctx: int) -> None:
+    _lib.bm_destroy(ctx)
+
+
+def make_dims(*, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim, dtype,
+              sm_scale=0.0) -> bm_dims:
+    dt = {"f32": BM_F32, "bf16": BM_BF16}.get(dtype, dtype)
+    return bm_dims(b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim, dt, sm_scale)
+
+
+# ---------------------------------------------------------------------------
+# tensor-owning convenience wrapper
+# ---------------------------------------------------------------------------
+class PDAttention:
+    """Owns one layer's bounded cache (torch tensors on a GPU) and drives the ABI.
+
+    Tensors passed to the calls have the sequence as dimension 2:
+    q, o ``[b, n_heads, T, d]`` and k, v ``[b, n_kv_heads, T, d]``, contiguous,
+    of the configured dtype, on the cache's device.  ``row`` selects the first
+    row of the block (prefill) or the step's row (decode) inside them.
+    """
+
+    def __init__(self, *, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim,
+                 dtype="bf16", sm_scale=0.0, device="cuda", init=True):
+        import torch
+
+        self.torch = torch
+        self.dims = make_dims(b=b, s=s, kv_max=kv_max, block=block, max_gen=max_gen,
+                              n_heads=n_heads, n_kv_heads=n_kv_heads, head_dim=head_dim,
+                              dtype=dtype, sm_scale=sm_scale)
+        bm_validate_dims(self.dims)
+        self.tdtype = torch.float32 if self.dims.dtype == BM_F32 else torch.bfloat16
+        self.device = torch.device(device)
+        self.cap = bm_cache_slots(self.dims)
+        self.group = n_heads // n_kv_heads
+        U = b * n_kv_heads
+        self.k = torch.empty((b, n_kv_heads, self.cap, head_dim), dtype=self.tdtype, device=self.device)
+        self.v = torch.empty_like(self.k)
+        self.score = torch.empty((b, n_kv_heads, self.cap), dtype=torch.float32, device=self.device)
+        self.pos = torch.zeros((b, n_kv_heads, self.cap), dtype=torch.int32, device=self.device)
+        self.len = torch.empty((b, n_kv_heads), dtype=torch.int32, device=self.device)
+        self.work_bytes = bm_workspace_bytes(self.dims)
+        self.work = torch.empty(self.work_bytes, dtype=torch.uint8, device=self.device)
+        self.cache = bm_cache(self.k.data_ptr(), self.v.data_ptr(), self.score.data_ptr(),
+                              self.pos.data_ptr(), self.len.data_ptr(), self.work.data_ptr(),
+                              self.work_bytes)
+        self.units = U
+        self.ctx = None
+        if init:
+            self.reset()
+
+    # -- helpers ----------------------------------------------------------------
+    def _stream(self) -> int:
+        return self.torch.cuda.current_stream(self.device).cuda_stream
+
+    def _check_tensor(self, x, heads, name):
+        t = self.torch
+        if x.device != self.device or x.dtype != self.tdtype or not x.is_contiguous():
+            raise ValueError(f"{name}: need a contiguous {self.tdtype} tensor on {self.device}")
+        if x.dim() != 4 or x.shape[0] != self.dims.b or x.shape[1] != heads or \
+                x.shape[3] != self.dims.head_dim:
+            raise ValueError(f"{name}: shape {tuple(x.shape)} is not [b, {heads}, T, d]")
+        return x
+
+    def _row_ptr(self, x, row):
+        if not 0 <= row < x.shape[2]:
+            raise ValueError(f"row {row} outside the tensor's {x.shape[2]} rows")
+        return x.data_ptr() + row * x.shape[3] * x.element_size()
+
+    # -- schedule ---------------------------------------------------------------
+    def reset(self) -> None:
+        if self.ctx is not None:
+            bm_destroy(self.ctx)
+        self.ctx = bm_init(self.dims, self.cache, self._stream())
+
+    def resume(self, length: int, next_pos: int) -> None:
+        if self.ctx is not None:
+            bm_destroy(self.ctx)
+        self.ctx = bm_resume(self.dims, self.cache, length, next_pos)
+
+    def prefill_block(self, t0, n_tok, q, k, v, o, row=None) -> None:
+        row = t0 if row is None else row
+        H, Hk = self.dims.n_heads, self.dims.n_kv_heads
+        for x, hh, nm in ((q, H, "q"), (k, Hk, "k"), (v, Hk, "v"), (o, H, "o")):
+            self._check_tensor(x, hh, nm)
+            if row + n_tok > x.shape[2]:
+                raise ValueError(f"{nm}: rows [{row}, {row + n_tok}) exceed {x.shape[2]}")
+        T = q.shape[2]
+        if not (k.shape[2] == v.shape[2] == o.shape[2] == T):
+            raise ValueError("q, k, v and o need the same number of rows")
+        bm_prefill_block(self.ctx, t0, n_tok, self._row_ptr(q, row), self._row_ptr(k, row),
+                         self._row_ptr(v, row), self._row_ptr(o, row), T, self._stream())
+
+    def evict_compact(self, curr_id) -> None:
+        bm_evict_compact(self.ctx, curr_id, self._stream())
+
+    def decode_step(self, pos, q, k, v, o, row=0) -> None:
+        H, Hk = self.dims.n_heads, self.dims.n_kv_heads
+        for x, hh, nm in ((q, H, "q"), (k, Hk, "k"), (v, Hk, "v"), (o, H, "o")):
+            self._check_tensor(x, hh, nm)
+        T = q.shape[2]
+        if not (k.shape[2] == v.shape[2] == o.shape[2] == T):
+            raise ValueError("q, k, v and o need the same number of rows")
+        bm_decode_step(self.ctx, pos, self._row_ptr(q, row), self._row_ptr(k, row),
+                       self._row_ptr(v, row), self._row_ptr(o, row), T, self._stream())
+
+    def run_prefill(self, q, k, v, o) -> None:
+        """Algorithm 1 prefill under the block loop: every block, then a cut."""
+        s, B = self.dims.s, self.dims.block
+        for t0 in range(0, s, B):
+            n = min(B, s - t0)
+            self.prefill_block(t0, n, q, k, v, o)
+            self.evict_compact(t0 + n - 1)
+
+    def run_decode(self, q, k, v, o, steps=None, first_row=None) -> None:
+        """Decode steps at positions s, s+1, ... using rows first_row.. (default s)."""
+        s = self.dims.s
+        steps = self.dims.max_gen if steps is None else steps
+        r0 = s if first_row is None else first_row
+        for t in range(steps):
+            self.decode_step(s + t, q, k, v, o, row=r0 + t)
+
+    @property
+    def length(self) -> int:
+        return bm_ctx_len(self.ctx)
+
+    @property
+    def next_pos(self) -> int:
+        return bm_ctx_next_pos(self.ctx)
+
+    def close(self) -> None:
+        if self.ctx is not None:
+            bm_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------------------
+# algorithmic work (used by the benchmark's roofline figures)
+# ---------------------------------------------------------------------------
+def prefill_flops(*, b, n_kv_heads, group, head_dim, s, kv_max, block) -> int:
+    """QK^T + PV flops the method must do: 4 d G per visible (query, key) pair."""
+    total = 0
+    length = 0
+    for t0 in range(0, s, block):
+        n = min(block, s - t0)
+        # row r of the block sees length + r + 1 entries
+        total += n * length + n * (n + 1) // 2
+        length = min(kv_max, length + n)
+    return 4 * head_dim * group * total * b * n_kv_heads
+
+
+def decode_bytes_per_step(*, b, n_kv_heads, group, head_dim, kv_max, elem_bytes) -> int:
+    """HBM bytes one decode step must move per the fused design: read the K̄
+    cached K and V rows, scores and positions; write K̄ scores, one K/V row,
+    one score and position; read q (G rows), k and v of the step; write o."""
+    d, G, es = head_dim, group, elem_bytes
+    per_unit = (2 * kv_max * d * es          # cached K and V
+                + kv_max * 4 * 2             # scores read and written
+                + kv_max * 4                 # positions
+                + (G + 2) * d * es           # q, new k, new v
+                + G * d * es                 # o
+                + 2 * d * es + 8)            # evicted slot overwrite (K, V, score, pos)
+    return per_unit * b * n_kv_heads

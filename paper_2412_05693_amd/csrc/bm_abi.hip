@@ -1,0 +1,367 @@
+// Host side of the C ABI declared in include/batchmax.h: argument, capacity and
+// order checks (all before any HIP call), the host copy of the schedule state,
+// and kernel launches on the caller's stream.  No device allocation, no stream
+// synchronisation, no exception crosses the boundary.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <new>
+#include <string>
+
+#include "bm_internal.h"
+
+#define BM_EXPORT extern "C" __attribute__((visibility("default")))
+
+struct bm_ctx {
+  bm_dims dims;
+  bm_cache cache;
+  int group;
+  int cap;
+  int units;
+  int elem_bytes;
+  float sm_scale;
+  bm::Layout lay;
+  int32_t len;        // live entries per unit (the same for every unit)
+  int32_t next_pos;   // next position the schedule expects
+  int32_t last_pos;   // last processed position, -1 before the first
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+
+int ok() {
+  g_err.clear();
+  return BM_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int check_dims(const bm_dims* d) {
+  if (!d) return fail(BM_ERR_INVALID_ARG, "dims is null");
+  if (d->b < 1 || d->s < 1 || d->kv_max < 1 || d->block < 1 || d->max_gen < 0 ||
+      d->n_heads < 1 || d->n_kv_heads < 1 || d->head_dim < 1)
+    return fail(BM_ERR_INVALID_ARG,
+                "sizes must be positive (b=%d s=%d kv_max=%d block=%d max_gen=%d H=%d Hk=%d d=%d)",
+                d->b, d->s, d->kv_max, d->block, d->max_gen, d->n_heads, d->n_kv_heads,
+                d->head_dim);
+  if (d->n_heads % d->n_kv_heads != 0)
+    return fail(BM_ERR_INVALID_ARG, "n_heads (%d) is not a multiple of n_kv_heads (%d)",
+                d->n_heads, d->n_kv_heads);
+  if (!(d->sm_scale >= 0.0f) || !std::isfinite(d->sm_scale))
+    return fail(BM_ERR_INVALID_ARG, "sm_scale must be finite and >= 0");
+  if ((int64_t)d->s + d->max_gen > (1 << 30))
+    return fail(BM_ERR_INVALID_ARG, "s + max_gen too large");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(BM_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", d->head_dim);
+  if (d->dtype != BM_F32 && d->dtype != BM_BF16)
+    return fail(BM_ERR_UNSUPPORTED, "dtype %d unsupported", d->dtype);
+  const int g = d->n_heads / d->n_kv_heads;
+  if (g != 1 && g != 2 && g != 4)
+    return fail(BM_ERR_UNSUPPORTED, "query heads per KV head %d unsupported (1, 2 or 4)", g);
+  if (d->block > bm::kMaxBlock)
+    return fail(BM_ERR_UNSUPPORTED, "block %d exceeds %d", d->block, bm::kMaxBlock);
+  if ((int64_t)d->kv_max + d->block > bm::kMaxCap)
+    return fail(BM_ERR_UNSUPPORTED, "kv_max + block = %lld exceeds %d",
+                (long long)d->kv_max + d->block, bm::kMaxCap);
+  if ((int64_t)d->b * d->n_kv_heads > (1 << 24))
+    return fail(BM_ERR_UNSUPPORTED, "b * n_kv_heads too large");
+  return BM_OK;
+}
+
+float eff_scale(const bm_dims& d) {
+  return d.sm_scale > 0.0f ? d.sm_scale : 1.0f / std::sqrt((float)d.head_dim);
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(BM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+namespace bm {
+
+Layout workspace_layout(const bm_dims& d) {
+  Layout l;
+  const int g = d.n_heads / d.n_kv_heads;
+  const int pt = positions_per_wg(g);
+  const size_t cap = (size_t)d.kv_max + d.block;
+  const size_t units = (size_t)d.b * d.n_kv_heads;
+  l.npt = (d.block + pt - 1) / pt;
+  size_t off = 0;
+  l.partial_off = off;
+  off = align256(off + units * l.npt * cap * sizeof(float));
+  l.holes_off = off;
+  off = align256(off + units * cap * sizeof(int32_t));
+  l.srcs_off = off;
+  off = align256(off + units * cap * sizeof(int32_t));
+  l.mcount_off = off;
+  off = align256(off + units * sizeof(int32_t));
+  l.total = off;
+  return l;
+}
+
+}  // namespace bm
+
+BM_EXPORT int bm_abi_version(void) { return BM_ABI_VERSION; }
+
+BM_EXPORT const char* bm_last_error(void) { return g_err.c_str(); }
+
+BM_EXPORT int bm_validate_dims(const bm_dims* dims) {
+  const int st = check_dims(dims);
+  return st == BM_OK ? ok() : st;
+}
+
+BM_EXPORT int32_t bm_cache_slots(const bm_dims* dims) {
+  if (check_dims(dims) != BM_OK) return -1;
+  return dims->kv_max + dims->block;
+}
+
+BM_EXPORT size_t bm_workspace_bytes(const bm_dims* dims) {
+  if (check_dims(dims) != BM_OK) return 0;
+  return bm::workspace_layout(*dims).total;
+}
+
+namespace {
+
+int make_ctx(const bm_dims* dims, const bm_cache* cache, bm_ctx** out) {
+  int st = check_dims(dims);
+  if (st != BM_OK) return st;
+  if (!cache || !out) return fail(BM_ERR_INVALID_ARG, "cache or out is null");
+  if (!cache->k || !cache->v || !cache->score || !cache->pos || !cache->len || !cache->work)
+    return fail(BM_ERR_INVALID_ARG, "a cache pointer is null");
+  if (((uintptr_t)cache->k | (uintptr_t)cache->v | (uintptr_t)cache->work) & 15)
+    return fail(BM_ERR_INVALID_ARG, "k, v and work must be 16-byte aligned");
+  if (((uintptr_t)cache->score | (uintptr_t)cache->pos | (uintptr_t)cache->len) & 3)
+    return fail(BM_ERR_INVALID_ARG, "score, pos and len must be 4-byte aligned");
+  const bm::Layout lay = bm::workspace_layout(*dims);
+  if (cache->work_bytes < lay.total)
+    return fail(BM_ERR_INVALID_ARG, "work_bytes %zu < required %zu", cache->work_bytes, lay.total);
+  bm_ctx* c = new (std::nothrow) bm_ctx;
+  if (!c) return fail(BM_ERR_INVALID_ARG, "out of host memory");
+  c->dims = *dims;
+  c->cache = *cache;
+  c->group = dims->n_heads / dims->n_kv_heads;
+  c->cap = dims->kv_max + dims->block;
+  c->units = dims->b * dims->n_kv_heads;
+  c->elem_bytes = dims->dtype == BM_BF16 ? 2 : 4;
+  c->sm_scale = eff_scale(*dims);
+  c->lay = lay;
+  c->len = 0;
+  c->next_pos = 0;
+  c->last_pos = -1;
+  *out = c;
+  return BM_OK;
+}
+
+char* work_at(const bm_ctx* c, size_t off) { return static_cast<char*>(c->cache.work) + off; }
+
+}  // namespace
+
+BM_EXPORT int bm_init(const bm_dims* dims, const bm_cache* cache, hipStream_t stream,
+                      bm_ctx** out) {
+  if (out) *out = nullptr;
+  bm_ctx* c = nullptr;
+  const int st = make_ctx(dims, cache, &c);
+  if (st != BM_OK) return st;
+  const size_t n_score = (size_t)c->units * c->cap;
+  const hipError_t e = bm::launch_reset(cache->score, cache->len, n_score, (size_t)c->units, stream);
+  if (e != hipSuccess) {
+    delete c;
+    return hip_fail(e, "reset launch");
+  }
+  *out = c;
+  return ok();
+}
+
+BM_EXPORT int bm_resume(const bm_dims* dims, const bm_cache* cache, int32_t len,
+                        int32_t next_pos, bm_ctx** out) {
+  if (out) *out = nullptr;
+  bm_ctx* c = nullptr;
+  const int st = make_ctx(dims, cache, &c);
+  if (st != BM_OK) return st;
+  if (len < 0 || len > c->cap || next_pos < 0 || next_pos > dims->s + dims->max_gen ||
+      len > next_pos) {
+    delete c;
+    return fail(BM_ERR_INVALID_ARG, "resume state len=%d next_pos=%d is not reachable", len,
+                next_pos);
+  }
+  c->len = len;
+  c->next_pos = next_pos;
+  c->last_pos = next_pos - 1;
+  *out = c;
+  return ok();
+}
+
+BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q,
+                               const void* k, const void* v, void* o, int32_t seq_ld,
+                               hipStream_t stream) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (!q || !k || !v || !o) return fail(BM_ERR_INVALID_ARG, "q, k, v or o is null");
+  if (n_tok < 1 || n_tok > ctx->dims.block)
+    return fail(BM_ERR_INVALID_ARG, "n_tok %d outside [1, block=%d]", n_tok, ctx->dims.block);
+  if (seq_ld < n_tok) return fail(BM_ERR_INVALID_ARG, "seq_ld %d < n_tok %d", seq_ld, n_tok);
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o) & 15)
+    return fail(BM_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+  if (t0 != ctx->next_pos)
+    return fail(BM_ERR_ORDER, "prefill t0=%d but the next position is %d", t0, ctx->next_pos);
+  if ((int64_t)t0 + n_tok > ctx->dims.s)
+    return fail(BM_ERR_ORDER, "block [%d, %d) runs past the prompt length s=%d", t0, t0 + n_tok,
+                ctx->dims.s);
+  if (ctx->len > ctx->dims.kv_max)
+    return fail(BM_ERR_ORDER, "cache holds %d > kv_max=%d entries: evict before the next block",
+                ctx->len, ctx->dims.kv_max);
+  if (ctx->len + n_tok > ctx->cap)
+    return fail(BM_ERR_CAPACITY, "len %d + n_tok %d exceeds cap %d", ctx->len, n_tok, ctx->cap);
+
+  bm::PrefillArgs a;
+  a.q = q;
+  a.kin = k;
+  a.vin = v;
+  a.o = o;
+  a.kc = ctx->cache.k;
+  a.vc = ctx->cache.v;
+  a.pos = ctx->cache.pos;
+  a.score = ctx->cache.score;
+  a.len = ctx->cache.len;
+  a.partial = reinterpret_cast<float*>(work_at(ctx, ctx->lay.partial_off));
+  a.seq_ld = seq_ld;
+  a.n_heads = ctx->dims.n_heads;
+  a.n_kv_heads = ctx->dims.n_kv_heads;
+  a.cap = ctx->cap;
+  a.len0 = ctx->len;
+  a.n_tok = n_tok;
+  a.t0 = t0;
+  const int ppw = bm::positions_per_wg(ctx->group);
+  a.npt_used = (n_tok + ppw - 1) / ppw;
+  a.npt_stride = ctx->lay.npt;
+  a.units = ctx->units;
+  a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
+  hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  e = bm::launch_score_reduce(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "score reduce launch");
+  ctx->len += n_tok;
+  ctx->next_pos = t0 + n_tok;
+  ctx->last_pos = t0 + n_tok - 1;
+  return ok();
+}
+
+BM_EXPORT int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (curr_id != ctx->last_pos)
+    return fail(BM_ERR_ORDER, "curr_id=%d but the last processed position is %d", curr_id,
+                ctx->last_pos);
+  if (ctx->len <= ctx->dims.kv_max) return ok();
+  bm::EvictArgs a;
+  a.kc = ctx->cache.k;
+  a.vc = ctx->cache.v;
+  a.score = ctx->cache.score;
+  a.pos = ctx->cache.pos;
+  a.len = ctx->cache.len;
+  a.holes = reinterpret_cast<int32_t*>(work_at(ctx, ctx->lay.holes_off));
+  a.srcs = reinterpret_cast<int32_t*>(work_at(ctx, ctx->lay.srcs_off));
+  a.mcount = reinterpret_cast<int32_t*>(work_at(ctx, ctx->lay.mcount_off));
+  a.cap = ctx->cap;
+  a.n = ctx->len;
+  a.kv_max = ctx->dims.kv_max;
+  a.curr_id = curr_id;
+  a.units = ctx->units;
+  a.head_dim = ctx->dims.head_dim;
+  a.elem_bytes = ctx->elem_bytes;
+  hipError_t e = bm::launch_select(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "select launch");
+  const int n_evict = ctx->len - ctx->dims.kv_max;
+  const int max_moves = n_evict < ctx->dims.kv_max ? n_evict : ctx->dims.kv_max;
+  e = bm::launch_compact(a, max_moves, stream);
+  if (e != hipSuccess) return hip_fail(e, "compact launch");
+  ctx->len = ctx->dims.kv_max;
+  return ok();
+}
+
+BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void* k,
+                             const void* v, void* o, int32_t seq_ld, hipStream_t stream) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (!q || !k || !v || !o) return fail(BM_ERR_INVALID_ARG, "q, k, v or o is null");
+  if (seq_ld < 1) return fail(BM_ERR_INVALID_ARG, "seq_ld %d < 1", seq_ld);
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o) & 15)
+    return fail(BM_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+  if (pos != ctx->next_pos)
+    return fail(BM_ERR_ORDER, "decode pos=%d but the next position is %d", pos, ctx->next_pos);
+  if (pos < ctx->dims.s)
+    return fail(BM_ERR_ORDER, "decode at pos=%d before the prompt (s=%d) is processed", pos,
+                ctx->dims.s);
+  if ((int64_t)pos >= (int64_t)ctx->dims.s + ctx->dims.max_gen)
+    return fail(BM_ERR_ORDER, "decode pos=%d beyond s + max_gen = %d", pos,
+                ctx->dims.s + ctx->dims.max_gen);
+  if (ctx->len > ctx->dims.kv_max)
+    return fail(BM_ERR_CAPACITY, "cache holds %d > kv_max=%d entries: evict after the last block",
+                ctx->len, ctx->dims.kv_max);
+  bm::DecodeArgs a;
+  a.q = q;
+  a.kin = k;
+  a.vin = v;
+  a.o = o;
+  a.kc = ctx->cache.k;
+  a.vc = ctx->cache.v;
+  a.score = ctx->cache.score;
+  a.pos = ctx->cache.pos;
+  a.len = ctx->cache.len;
+  a.seq_ld = seq_ld;
+  a.n_heads = ctx->dims.n_heads;
+  a.n_kv_heads = ctx->dims.n_kv_heads;
+  a.cap = ctx->cap;
+  a.len0 = ctx->len;
+  a.kv_max = ctx->dims.kv_max;
+  a.cur_pos = pos;
+  a.units = ctx->units;
+  a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
+  const hipError_t e =
+      bm::launch_decode(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  if (ctx->len < ctx->dims.kv_max) ctx->len += 1;
+  ctx->next_pos = pos + 1;
+  ctx->last_pos = pos;
+  return ok();
+}
+
+BM_EXPORT int32_t bm_ctx_len(const bm_ctx* ctx) { return ctx ? ctx->len : -1; }
+
+BM_EXPORT int32_t bm_ctx_next_pos(const bm_ctx* ctx) { return ctx ? ctx->next_pos : -1; }
+
+BM_EXPORT void bm_destroy(bm_ctx* ctx) { delete ctx; }
+
+// ---------------------------------------------------------------------------
+// cache reset: a fill kernel rather than hipMemsetAsync, so the enqueued work
+// is safe to record into a HIP graph
+// ---------------------------------------------------------------------------
+namespace bm {
+namespace {
+__global__ void reset_kernel(float* score, int32_t* len, size_t n_score, size_t n_len) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_score; i += stride)
+    score[i] = 0.0f;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_len; i += stride) len[i] = 0;
+}
+}  // namespace
+
+hipError_t launch_reset(float* score, int32_t* len, size_t n_score, size_t n_len,
+                        hipStream_t stream) {
+  size_t blocks = (n_score + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(reset_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, score, len,
+                     n_score, n_len);
+  return hipGetLastError();
+}
+}  // namespace bm

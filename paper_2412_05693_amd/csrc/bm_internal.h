@@ -1,0 +1,91 @@
+// Internal declarations shared by the C-ABI host code and the HIP kernel files.
+// Not part of the public ABI (include/batchmax.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "batchmax.h"
+
+namespace bm {
+
+// Prefill attention tiling (gfx950: 64-wide waves, 32x32 MFMA tiles).
+// A workgroup has 4 waves; each wave owns 32 query rows of one query head, so a
+// workgroup covers 128 / G consecutive block positions of one unit for all G
+// heads of its group.  Keys stream through LDS in tiles of 64.
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRowsPerWave = 32;
+constexpr int kKeyTile = 64;
+constexpr int kMaxCap = 4096;
+constexpr int kMaxBlock = 1024;
+
+inline int positions_per_wg(int group) { return kWaves * kRowsPerWave / group; }
+
+// Workspace carve-up (all offsets 256-byte aligned).
+struct Layout {
+  int npt;              // prefill workgroups per unit for a full block
+  size_t partial_off;   // float  [U][npt][cap]  per-workgroup score column sums
+  size_t holes_off;     // int32  [U][cap]       evicted slots below kv_max, slot order
+  size_t srcs_off;      // int32  [U][cap]       surviving slots at or above kv_max
+  size_t mcount_off;    // int32  [U]            number of moves per unit
+  size_t total;
+};
+
+Layout workspace_layout(const bm_dims& d);
+
+struct PrefillArgs {
+  const void* q;      // row t0 of [b, H, seq_ld, D]
+  const void* kin;    // row t0 of [b, Hk, seq_ld, D]
+  const void* vin;
+  void* o;
+  void* kc;           // cache [U, cap, D]
+  void* vc;
+  int32_t* pos;       // [U, cap]
+  float* score;       // [U, cap]
+  int32_t* len;       // [U]
+  float* partial;     // [U, npt, cap]
+  int64_t seq_ld;
+  int n_heads, n_kv_heads, cap, len0, n_tok, t0, npt_used, npt_stride, units;
+  float scale_log2;   // sm_scale * log2(e)
+};
+
+struct EvictArgs {
+  void* kc;
+  void* vc;
+  float* score;
+  int32_t* pos;
+  int32_t* len;
+  int32_t* holes;
+  int32_t* srcs;
+  int32_t* mcount;
+  int cap, n, kv_max, curr_id, units, head_dim, elem_bytes;
+};
+
+struct DecodeArgs {
+  const void* q;      // [b, H, seq_ld, D] row of this step
+  const void* kin;    // [b, Hk, seq_ld, D]
+  const void* vin;
+  void* o;
+  void* kc;
+  void* vc;
+  float* score;
+  int32_t* pos;
+  int32_t* len;
+  int64_t seq_ld;
+  int n_heads, n_kv_heads, cap, len0, kv_max, cur_pos, units;
+  float scale_log2;
+};
+
+hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int group,
+                          hipStream_t stream);
+hipError_t launch_score_reduce(const PrefillArgs& a, hipStream_t stream);
+hipError_t launch_select(const EvictArgs& a, hipStream_t stream);
+hipError_t launch_compact(const EvictArgs& a, int max_moves, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group,
+                         hipStream_t stream);
+hipError_t launch_reset(float* score, int32_t* len, size_t n_score, size_t n_len,
+                        hipStream_t stream);
+
+}  // namespace bm

@@ -1,0 +1,320 @@
+// K4: one decode step per unit, fused: attention over the bounded cache plus
+// the step's own KV pair, score update, ranking, one eviction, in-place write.
+//
+// Decode is bandwidth-bound (the paper notes it reloads the whole cache every
+// step, Sec. 1): the kernel reads each cached K and V row exactly once.  One
+// workgroup per unit (sample, KV head); L = len + 1 entries (len cached slots
+// plus the step's pair, which sits in a virtual slot `len`).
+//   1. logits z[g][j] = sm_scale * q_g . k_j for the G query heads, kept in LDS
+//      (bf16: a 16x16x32 MFMA per 16 keys, K rows as the A operand straight
+//      from global memory; f32: VALU dot products);
+//   2. exact softmax per query head (max, sum, normalise) in LDS;
+//   3. score_j += sum_g P[g][j] (the sum_weights update of Sec. 3.2), ranking
+//      key ave = score / (pos_now + 1 - pos) packed with pos into 64 bits, and a
+//      workgroup argmin (older entry first on an exact tie);
+//   4. o_g = sum_j P[g][j] v_j on VALU, V rows read once, 16 bytes per lane;
+//   5. write back the scores; if the cache exceeds kv_max, the new pair takes
+//      the slot of the removed entry (or is dropped if it is the one removed);
+//      otherwise it is appended at slot len.
+#include <type_traits>
+
+#include "bm_internal.h"
+
+namespace bm {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ uint64_t rank_key(float score, int pos, int curr_id) {
+  const float ave = score / (float)(curr_id + 1 - pos);
+  return ((uint64_t)__float_as_uint(ave) << 32) | (uint32_t)pos;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int off) {
+  const uint32_t lo = __shfl_xor((uint32_t)x, off);
+  const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), off);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+template <bool BF16, int D, int G>
+__global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
+  using E = typename std::conditional<BF16, uint16_t, float>::type;
+  constexpr int EPC = 16 / sizeof(E);       // elements per 16-byte chunk
+  constexpr int CPR = D / EPC;              // 16-byte chunks per row
+  extern __shared__ float dsm[];
+  __shared__ uint64_t s_wkey[4];
+  __shared__ int s_wslot[4];
+
+  const int u = blockIdx.x;
+  const int bi = u / a.n_kv_heads, hk = u - (u / a.n_kv_heads) * a.n_kv_heads;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int len0 = a.len0;
+  const int L = len0 + 1;
+  const int Lp = (L + 3) & ~3;
+  float* P = dsm;                 // [G][Lp] logits, then probabilities
+  float* sc = P + G * Lp;         // [Lp] updated scores
+  float* red = sc + Lp;           // [4][G][D] partial outputs per wave
+
+  const E* kc = static_cast<const E*>(a.kc) + (int64_t)u * a.cap * D;
+  const E* vc = static_cast<const E*>(a.vc) + (int64_t)u * a.cap * D;
+  const int64_t plane = ((int64_t)bi * a.n_kv_heads + hk) * a.seq_ld;
+  const E* knew = static_cast<const E*>(a.kin) + plane * D;
+  const E* vnew = static_cast<const E*>(a.vin) + plane * D;
+  const E* qbase = static_cast<const E*>(a.q) + ((int64_t)bi * a.n_heads + hk * G) * a.seq_ld * D;
+  const float c2 = a.scale_log2;
+
+  // ---------------- 1. logits ----------------
+  if constexpr (BF16) {
+    const int col = lane & 15, g4 = lane >> 4;
+    bf16x8 qop[D / 32];
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      u32x4 qw = {0, 0, 0, 0};
+      if (col < G)
+        qw = *reinterpret_cast<const u32x4*>(qbase + (int64_t)col * a.seq_ld * D + 32 * ks + 8 * g4);
+      qop[ks] = __builtin_bit_cast(bf16x8, qw);
+    }
+    const int ngroups = (L + 15) / 16;
+#pragma unroll 2
+    for (int kg = w; kg < ngroups; kg += 4) {
+      const int key = kg * 16 + col;
+      const E* src = key < len0 ? kc + (int64_t)key * D : (key == len0 ? knew : nullptr);
+      u32x4 kw[D / 32];
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks)
+        kw[ks] = src ? *reinterpret_cast<const u32x4*>(src + 32 * ks + 8 * g4) : u32x4{0, 0, 0, 0};
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kw[ks]), qop[ks],
+                                                      acc, 0, 0, 0);
+      if (col < G) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int kk = kg * 16 + 4 * g4 + j;
+          if (kk < L) P[col * Lp + kk] = acc[j] * c2;
+        }
+      }
+    }
+  } else {
+    constexpr int CH = D / 4;               // float4 chunks per row
+    constexpr int NKL = 256 / CH;           // keys in flight per workgroup pass
+    const int c = tid % CH, kl = tid / CH;
+    float4 qr[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      qr[g] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(qbase) +
+                                               (int64_t)g * a.seq_ld * D + 4 * c);
+    const int iters = (L + NKL - 1) / NKL;
+    for (int it = 0; it < iters; ++it) {
+      const int j = kl + it * NKL;
+      const float* src = j < len0 ? reinterpret_cast<const float*>(kc) + (int64_t)j * D
+                                  : (j == len0 ? reinterpret_cast<const float*>(knew) : nullptr);
+      const float4 kv = src ? *reinterpret_cast<const float4*>(src + 4 * c) : make_float4(0, 0, 0, 0);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float part = qr[g].x * kv.x + qr[g].y * kv.y + qr[g].z * kv.z + qr[g].w * kv.w;
+#pragma unroll
+        for (int off = CH / 2; off > 0; off >>= 1) part += __shfl_xor(part, off);
+        if (c == 0 && j < L) P[g * Lp + j] = part * c2;
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---------------- 2. softmax per query head ----------------
+  for (int g = w; g < G; g += 4) {
+    float* pg = P + g * Lp;
+    float m = kNegInf;
+    for (int j = lane; j < L; j += 64) m = fmaxf(m, pg[j]);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    float s = 0.0f;
+    for (int j = lane; j < L; j += 64) {
+      const float e = __builtin_amdgcn_exp2f(pg[j] - m);
+      pg[j] = e;
+      s += e;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    const float inv = 1.0f / s;
+    for (int j = lane; j < L; j += 64) pg[j] *= inv;
+  }
+  __syncthreads();
+
+  // ---------------- 3. scores and ranking ----------------
+  const bool evict = L > a.kv_max;
+  {
+    const float* score = a.score + (int64_t)u * a.cap;
+    const int32_t* pos = a.pos + (int64_t)u * a.cap;
+    uint64_t best = ~0ull;
+    int bslot = -1;
+    for (int j = tid; j < L; j += 256) {
+      float ps = 0.0f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
+      const float s = (j < len0 ? score[j] : 0.0f) + ps;
+      sc[j] = s;
+      const int pj = j < len0 ? pos[j] : a.cur_pos;
+      const uint64_t key = rank_key(s, pj, a.cur_pos);
+      if (key < best) {
+        best = key;
+        bslot = j;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const uint64_t ob = shfl_xor_u64(best, off);
+      const int os = __shfl_xor(bslot, off);
+      if (ob < best) {
+        best = ob;
+        bslot = os;
+      }
+    }
+    if (lane == 0) {
+      s_wkey[w] = best;
+      s_wslot[w] = bslot;
+    }
+  }
+
+  // ---------------- 4. outputs o_g = sum_j P[g][j] v_j ----------------
+  {
+    constexpr int NKL = 256 / CPR;
+    constexpr int UNR = 4;
+    const int c = tid % CPR, kl = tid / CPR;
+    float acc[G][EPC];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[g][e] = 0.0f;
+    for (int j0 = kl; j0 < L; j0 += NKL * UNR) {
+      u32x4 vw[UNR];
+#pragma unroll
+      for (int r = 0; r < UNR; ++r) {
+        const int j = j0 + r * NKL;
+        const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
+        vw[r] = src ? *reinterpret_cast<const u32x4*>(src + c * EPC) : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int r = 0; r < UNR; ++r) {
+        const int j = j0 + r * NKL;
+        if (j >= L) break;
+        float vf[EPC];
+        if constexpr (BF16) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            vf[2 * e] = __uint_as_float(vw[r][e] << 16);
+            vf[2 * e + 1] = __uint_as_float(vw[r][e] & 0xffff0000u);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) vf[e] = __uint_as_float(vw[r][e]);
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float p = P[g * Lp + j];
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+        }
+      }
+    }
+    // reduce the lanes of a wave that share chunk c, then across waves in LDS
+#pragma unroll
+    for (int off = CPR; off < 64; off <<= 1)
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+    if (lane < CPR) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) red[(w * G + g) * D + c * EPC + e] = acc[g][e];
+    }
+  }
+  __syncthreads();
+
+  // final outputs
+  for (int idx = tid; idx < G * D; idx += 256) {
+    const int g = idx / D, d = idx - g * D;
+    const float x = red[(0 * G + g) * D + d] + red[(1 * G + g) * D + d] +
+                    red[(2 * G + g) * D + d] + red[(3 * G + g) * D + d];
+    E* o = static_cast<E*>(a.o) + (((int64_t)bi * a.n_heads + hk * G + g) * a.seq_ld) * D + d;
+    if constexpr (BF16) {
+      *o = __builtin_bit_cast(uint16_t, (__bf16)x);
+    } else {
+      *o = x;
+    }
+  }
+
+  // ---------------- 5. write back ----------------
+  int e_slot = -1;
+  if (evict) {
+    uint64_t best = s_wkey[0];
+    e_slot = s_wslot[0];
+#pragma unroll
+    for (int i = 1; i < 4; ++i)
+      if (s_wkey[i] < best) {
+        best = s_wkey[i];
+        e_slot = s_wslot[i];
+      }
+  }
+  const int dst = evict ? e_slot : len0;          // slot that receives the new pair
+  float* score = a.score + (int64_t)u * a.cap;
+  for (int j = tid; j < len0; j += 256)
+    if (j != dst) score[j] = sc[j];
+  if (dst >= 0 && dst < len0 + (evict ? 0 : 1)) {
+    E* kd = static_cast<E*>(a.kc) + ((int64_t)u * a.cap + dst) * D;
+    E* vd = static_cast<E*>(a.vc) + ((int64_t)u * a.cap + dst) * D;
+    for (int cidx = tid; cidx < 2 * CPR; cidx += 256) {
+      const int which = cidx / CPR, cc = cidx - which * CPR;
+      const u32x4 x = *reinterpret_cast<const u32x4*>((which ? vnew : knew) + cc * EPC);
+      *reinterpret_cast<u32x4*>((which ? vd : kd) + cc * EPC) = x;
+    }
+    if (tid == 0) {
+      score[dst] = sc[len0];
+      a.pos[(int64_t)u * a.cap + dst] = a.cur_pos;
+    }
+  }
+  if (tid == 0) a.len[u] = evict ? len0 : len0 + 1;
+}
+
+template <bool BF16, int D, int G>
+hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
+  const int L = a.len0 + 1;
+  const int Lp = (L + 3) & ~3;
+  const size_t lds = sizeof(float) * ((size_t)G * Lp + Lp + 4 * G * D);
+  hipLaunchKernelGGL((decode_kernel<BF16, D, G>), dim3((unsigned)a.units), dim3(256), lds, stream,
+                     a);
+  return hipGetLastError();
+}
+
+template <bool BF16, int D>
+hipError_t launch_g(const DecodeArgs& a, int group, hipStream_t stream) {
+  switch (group) {
+    case 1: return launch_t<BF16, D, 1>(a, stream);
+    case 2: return launch_t<BF16, D, 2>(a, stream);
+    case 4: return launch_t<BF16, D, 4>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group,
+                         hipStream_t stream) {
+  if (dtype == BM_BF16) {
+    if (head_dim == 128) return launch_g<true, 128>(a, group, stream);
+    if (head_dim == 64) return launch_g<true, 64>(a, group, stream);
+  } else if (dtype == BM_F32) {
+    if (head_dim == 128) return launch_g<false, 128>(a, group, stream);
+    if (head_dim == 64) return launch_g<false, 64>(a, group, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace bm

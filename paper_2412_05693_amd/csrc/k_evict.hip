@@ -1,0 +1,186 @@
+// K2 + K3: cut every unit back to kv_max entries and compact in place.
+//
+// K2 (select_kernel), one workgroup per unit: every live entry j gets the
+// ranking key of Sec. 3.2, ave_j = score_j / (curr_id + 1 - pos_j) in IEEE
+// float32 division, packed with its position into one 64-bit integer
+// (ave bits << 32 | pos).  ave >= 0, so the integer order is the order
+// (ave ascending, pos ascending): the smallest ave goes first and, on an exact
+// tie, the older entry (the tie rule of the oracle).  An 8-pass LDS radix
+// select over 8-bit digits finds the E-th smallest key exactly (positions are
+// unique, so exactly E keys are <= it).  Evicted slots below kv_max become
+// holes, surviving slots at or above kv_max become sources; both lists are
+// built in slot order with a workgroup prefix count, so the pairing is
+// deterministic.
+//
+// K3 (compact_kernel), units x chunks of 32 moves: the i-th source moves into
+// the i-th hole (K row, V row, score, pos), 16-byte coalesced copies.  Sources
+// and holes are disjoint, so moves never overlap.
+#include "bm_internal.h"
+
+namespace bm {
+namespace {
+
+constexpr int kMaxPer = kMaxCap / 256;  // keys per thread
+
+__device__ __forceinline__ uint64_t rank_key(float score, int pos, int curr_id) {
+  const float ave = score / (float)(curr_id + 1 - pos);
+  return ((uint64_t)__float_as_uint(ave) << 32) | (uint32_t)pos;
+}
+
+// exclusive prefix count of `flag` over the workgroup in thread order; returns
+// the workgroup total through *total
+__device__ __forceinline__ int block_excl_count(bool flag, int* s_wave, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t b = __ballot(flag);
+  const int in_wave = __popcll(b & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+  if (lane == 0) s_wave[w] = __popcll(b);
+  __syncthreads();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = s_wave[i];
+    before += (i < w) ? c : 0;
+    tot += c;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + in_wave;
+}
+
+__global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint64_t s_prefix;
+  __shared__ int s_need;
+  __shared__ int s_wave[4];
+  const int u = blockIdx.x;
+  const int tid = threadIdx.x;
+  const float* score = a.score + (int64_t)u * a.cap;
+  const int32_t* pos = a.pos + (int64_t)u * a.cap;
+  const int per = (a.n + 255) / 256;
+
+  uint64_t key[kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int j = tid + 256 * i;
+    key[i] = (i < per && j < a.n) ? rank_key(score[j], pos[j], a.curr_id) : ~0ull;
+  }
+
+  // radix select of the E-th smallest key (1-based)
+  uint64_t prefix = 0;
+  int need = a.n - a.kv_max;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    const uint64_t himask = pass == 0 ? 0ull : (~0ull << (shift + 8));
+    hist[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+      const int j = tid + 256 * i;
+      if (i < per && j < a.n && (key[i] & himask) == prefix)
+        atomicAdd(&hist[(key[i] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
+                     h3 = hist[4 * tid + 3];
+      const uint32_t mine = h0 + h1 + h2 + h3;
+      uint32_t incl = mine;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = __shfl_up(incl, off);
+        if (tid >= off) incl += o;
+      }
+      uint32_t ex = incl - mine;
+      const uint32_t hv[4] = {h0, h1, h2, h3};
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        if ((int)ex < need && need <= (int)(ex + hv[b])) {
+          s_prefix = prefix | ((uint64_t)(4 * tid + b) << shift);
+          s_need = need - (int)ex;
+        }
+        ex += hv[b];
+      }
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    need = s_need;
+  }
+  const uint64_t thr = prefix;  // exactly n - kv_max keys are <= thr
+
+  // holes (evicted, slot < kv_max) and sources (kept, slot >= kv_max), slot order
+  int32_t* holes = a.holes + (int64_t)u * a.cap;
+  int32_t* srcs = a.srcs + (int64_t)u * a.cap;
+  int hbase = 0, sbase = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    if (i >= per) break;  // uniform across the workgroup
+    const int j = tid + 256 * i;
+    const bool live = j < a.n;
+    const bool ev = live && key[i] <= thr;
+    const bool is_hole = live && j < a.kv_max && ev;
+    const bool is_src = live && j >= a.kv_max && !ev;
+    int ht, stot;
+    const int hr = block_excl_count(is_hole, s_wave, &ht);
+    const int sr = block_excl_count(is_src, s_wave, &stot);
+    if (is_hole) holes[hbase + hr] = j;
+    if (is_src) srcs[sbase + sr] = j;
+    hbase += ht;
+    sbase += stot;
+  }
+  if (tid == 0) {
+    a.mcount[u] = min(hbase, sbase);
+    a.len[u] = a.kv_max;
+  }
+}
+
+__global__ void __launch_bounds__(256) compact_kernel(EvictArgs a, int nchunks) {
+  constexpr int kMoves = 32;
+  const int u = blockIdx.x / nchunks;
+  const int chunk = blockIdx.x - u * nchunks;
+  const int m = a.mcount[u];
+  const int m0 = chunk * kMoves;
+  if (m0 >= m) return;
+  const int32_t* holes = a.holes + (int64_t)u * a.cap;
+  const int32_t* srcs = a.srcs + (int64_t)u * a.cap;
+  const int row_bytes = a.head_dim * a.elem_bytes;
+  const int cpr = row_bytes / 16;
+  char* kc = static_cast<char*>(a.kc) + (int64_t)u * a.cap * row_bytes;
+  char* vc = static_cast<char*>(a.vc) + (int64_t)u * a.cap * row_bytes;
+  const int total = kMoves * 2 * cpr;
+  for (int c = threadIdx.x; c < total; c += 256) {
+    const int mv = c / (2 * cpr);
+    const int rem = c - mv * 2 * cpr;
+    const int mi = m0 + mv;
+    if (mi >= m) continue;
+    const int which = rem / cpr, cc = rem - which * cpr;
+    char* base = which ? vc : kc;
+    const int64_t src = (int64_t)srcs[mi] * row_bytes + cc * 16;
+    const int64_t dst = (int64_t)holes[mi] * row_bytes + cc * 16;
+    *reinterpret_cast<uint4*>(base + dst) = *reinterpret_cast<const uint4*>(base + src);
+  }
+  if (threadIdx.x < kMoves) {
+    const int mi = m0 + threadIdx.x;
+    if (mi < m) {
+      const int s = srcs[mi], d = holes[mi];
+      a.score[(int64_t)u * a.cap + d] = a.score[(int64_t)u * a.cap + s];
+      a.pos[(int64_t)u * a.cap + d] = a.pos[(int64_t)u * a.cap + s];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const EvictArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const EvictArgs& a, int max_moves, hipStream_t stream) {
+  if (max_moves <= 0) return hipSuccess;
+  const int nchunks = (max_moves + 31) / 32;
+  hipLaunchKernelGGL(compact_kernel, dim3((unsigned)(a.units * nchunks)), dim3(256), 0, stream,
+                     a, nchunks);
+  return hipGetLastError();
+}
+
+}  // namespace bm

@@ -1,0 +1,174 @@
+"""GPU-versus-oracle comparison of a full P&D run, event by event.
+
+Both sides get exactly the same input values (the seeded unit streams).  After
+every device call the checked units' state is copied back and compared with the
+float64 oracle stepping in lockstep:
+
+* cache length: exact;
+* the set of live positions after every cut: exact, except inside the near-tie
+  band -- if the device kept a different set, every entry it evicted must rank
+  within ``band`` (in the oracle's own averages) of every entry it kept; the
+  oracle then adopts the device's set so later steps stay comparable;
+* scores of live entries, matched by position: relative tolerance 1e-3;
+* attention outputs: max abs error <= 2e-2 (bf16) or 1e-4 (float32).
+
+Counts of cuts, near-ties (oracle gap below ``band``) and adopted sets are
+reported; any other difference is a failure.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from oracle import pd as opd
+from paper_2412_05693_amd import synth
+from paper_2412_05693_amd.batchmax import PDAttention
+
+BAND = 1e-6
+SCORE_RTOL = 1e-3
+SCORE_ATOL = 1e-6
+OUT_TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+@dataclass
+class Stats:
+    cuts: int = 0
+    near_ties: int = 0
+    adopted: int = 0
+    max_out_err: float = 0.0
+    max_score_rel: float = 0.0
+    failures: list = field(default_factory=list)
+
+    def fail(self, msg):
+        if len(self.failures) < 20:
+            self.failures.append(msg)
+
+    def summary(self) -> str:
+        return (f"cuts={self.cuts} near_ties={self.near_ties} adopted={self.adopted} "
+                f"max_out_err={self.max_out_err:.3e} max_score_rel={self.max_score_rel:.3e} "
+                f"failures={len(self.failures)}")
+
+
+def make_pd(wl: synth.Workload, device="cuda", b=None) -> PDAttention:
+    return PDAttention(b=wl.b if b is None else b, s=wl.s, kv_max=wl.kv_max, block=wl.block,
+                       max_gen=wl.n_decode, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads,
+                       head_dim=wl.head_dim, dtype=wl.dtype, sm_scale=wl.sm_scale, device=device)
+
+
+def _snapshot(pd: PDAttention, units, length):
+    bi = torch.tensor([u[0] for u in units], device=pd.device)
+    hk = torch.tensor([u[1] for u in units], device=pd.device)
+    pos = pd.pos[bi, hk, :length].cpu().numpy()
+    score = pd.score[bi, hk, :length].cpu().numpy().astype(np.float64)
+    dlen = pd.len[bi, hk].cpu().numpy()
+    return pos, score, dlen
+
+
+def _compare_state(tag, orc, pos, score, dlen, length, st: Stats):
+    if np.any(dlen != length):
+        st.fail(f"{tag}: device len {dlen.tolist()} != {length}")
+        return False
+    order = np.argsort(pos)
+    gpos, gscore = pos[order], score[order]
+    opos_order = np.argsort(orc.pos)
+    opos, oscore = orc.pos[opos_order], orc.score[opos_order]
+    if not np.array_equal(gpos, opos):
+        st.fail(f"{tag}: live positions differ (device {len(gpos)}, oracle {len(opos)})")
+        return False
+    err = np.abs(gscore - oscore)
+    rel = err / np.maximum(np.abs(oscore), 1e-30)
+    st.max_score_rel = max(st.max_score_rel, float(np.max(np.where(err > SCORE_ATOL, rel, 0.0))))
+    bad = err > SCORE_RTOL * np.abs(oscore) + SCORE_ATOL
+    if np.any(bad):
+        i = int(np.argmax(bad))
+        st.fail(f"{tag}: score of pos {gpos[i]} {gscore[i]:.8g} vs oracle {oscore[i]:.8g}")
+        return False
+    return True
+
+
+def _compare_cut(tag, orc: opd.StepOracle, ev, gpu_pos, st: Stats):
+    if ev is None:
+        return
+    st.cuts += 1
+    if ev.gap < BAND:
+        st.near_ties += 1
+    gk = sorted(int(p) for p in gpu_pos)
+    ok = list(int(p) for p in ev.kept_pos)
+    if gk == ok:
+        return
+    ave = {int(p): float(a) for p, a in zip(ev.all_pos, ev.all_ave)}
+    gset = set(gk)
+    if len(gk) != len(ok) or not gset <= set(ave):
+        st.fail(f"{tag}: device kept set is not a valid cut")
+        return
+    evicted = set(ave) - gset
+    spread = max(ave[p] for p in evicted) - min(ave[p] for p in gset)
+    if spread < BAND:
+        st.adopted += 1
+        orc.adopt(gk)
+    else:
+        st.fail(f"{tag}: device cut differs beyond the band (spread {spread:.3e}, "
+                f"oracle gap {ev.gap:.3e})")
+
+
+def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decode_steps=None,
+               inputs=None, pd=None, stop_on_failure=True) -> Stats:
+    """Run the whole P&D schedule on the device and compare the checked units."""
+    st = Stats()
+    if inputs is None:
+        inputs = synth.batch_inputs(wl, device, checked=checked, sharp=sharp)
+    q, k, v = inputs
+    o = torch.zeros_like(q)
+    pd = pd or make_pd(wl, device)
+    G = wl.group
+    uin = {u: synth.unit_inputs(wl, 0, u[0], u[1], sharp=sharp) for u in checked}
+    orcs = {u: opd.StepOracle(head_dim=wl.head_dim, group=G, kv_max=wl.kv_max,
+                              sm_scale=wl.sm_scale) for u in checked}
+    tol = OUT_TOL[wl.dtype]
+    D = wl.n_decode if decode_steps is None else decode_steps
+
+    def check_out(tag, u, rows, ref):
+        bi, hk = u
+        got = o[bi, hk * G:(hk + 1) * G, rows].float().cpu().numpy().astype(np.float64)
+        err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+        st.max_out_err = max(st.max_out_err, err)
+        if not err <= tol:
+            st.fail(f"{tag} unit {u}: output error {err:.3e} > {tol}")
+
+    for t0 in range(0, wl.s, wl.block):
+        n = min(wl.block, wl.s - t0)
+        pd.prefill_block(t0, n, q, k, v, o)
+        length = pd.length
+        pos, score, dlen = _snapshot(pd, checked, length)
+        for i, u in enumerate(checked):
+            uq, uk, uv = uin[u]
+            ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
+            check_out(f"block {t0}", u, slice(t0, t0 + n), ref)
+            _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st)
+        pd.evict_compact(t0 + n - 1)
+        length = pd.length
+        pos, score, dlen = _snapshot(pd, checked, length)
+        for i, u in enumerate(checked):
+            ev = orcs[u].evict(t0 + n - 1, "prefill")
+            _compare_cut(f"cut {t0 + n - 1} unit {u}", orcs[u], ev, pos[i], st)
+            _compare_state(f"cut {t0 + n - 1} unit {u}", orcs[u], pos[i], score[i], dlen[i],
+                           length, st)
+        if stop_on_failure and st.failures:
+            return st
+
+    for t in range(D):
+        p = wl.s + t
+        pd.decode_step(p, q, k, v, o, row=p)
+        length = pd.length
+        pos, score, dlen = _snapshot(pd, checked, length)
+        for i, u in enumerate(checked):
+            uq, uk, uv = uin[u]
+            ref, ev = orcs[u].decode_step(p, uq[:, p], uk[p], uv[p])
+            check_out(f"decode {p}", u, slice(p, p + 1), ref[:, None, :])
+            _compare_cut(f"decode {p} unit {u}", orcs[u], ev, pos[i], st)
+            _compare_state(f"decode {p} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st)
+        if stop_on_failure and st.failures:
+            return st
+    return st

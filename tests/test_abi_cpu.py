@@ -1,0 +1,194 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol,
+and every argument, capacity and order error is reported before any device
+work.  Contexts here come from bm_resume with placeholder addresses, which no
+call below ever dereferences: each call is one the host checks reject."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2412_05693_amd import batchmax as bmx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "batchmax.h")
+
+FAKE = 0x7F0000000000  # placeholder device address, 4 KiB aligned, never touched
+
+
+def dims(**kw):
+    base = dict(b=2, s=512, kv_max=128, block=64, max_gen=32, n_heads=8, n_kv_heads=2,
+                head_dim=128, dtype="bf16")
+    base.update(kw)
+    return bmx.make_dims(**base)
+
+
+def fake_cache(d):
+    return bmx.bm_cache(FAKE, FAKE + 0x1000000, FAKE + 0x2000000, FAKE + 0x3000000,
+                        FAKE + 0x4000000, FAKE + 0x5000000, bmx.bm_workspace_bytes(d))
+
+
+def status_of(fn, *args):
+    try:
+        fn(*args)
+    except bmx.BatchMaxError as e:
+        return e.status
+    return bmx.BM_OK
+
+
+def test_header_symbols_exported():
+    text = open(HEADER).read()
+    declared = sorted(set(re.findall(r"\b(bm_[a-z_]+)\s*\(", text)))
+    assert declared, "no declarations found"
+    lib = ctypes.CDLL(bmx.LIB_PATH)
+    for name in declared:
+        assert hasattr(lib, name), f"{name} declared but not exported"
+    assert sorted(bmx.EXPORTED) == declared
+
+
+def test_version_matches_header():
+    m = re.search(r"#define BM_ABI_VERSION (\d+)", open(HEADER).read())
+    assert bmx.bm_abi_version() == int(m.group(1))
+
+
+def test_slots_and_workspace():
+    d = dims()
+    assert bmx.bm_cache_slots(d) == 128 + 64
+    ws = bmx.bm_workspace_bytes(d)
+    # partial sums: units x ceil(block / (128 / G)) x cap floats, plus lists
+    U, cap, npt = 4, 192, 2
+    assert ws >= U * npt * cap * 4 + 2 * U * cap * 4 + U * 4
+    assert bmx.bm_cache_slots(dims(b=0)) == -1
+    assert bmx.bm_workspace_bytes(dims(head_dim=96)) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(b=0), bmx.BM_ERR_INVALID_ARG),
+    (dict(s=-1), bmx.BM_ERR_INVALID_ARG),
+    (dict(kv_max=0), bmx.BM_ERR_INVALID_ARG),
+    (dict(block=0), bmx.BM_ERR_INVALID_ARG),
+    (dict(max_gen=-1), bmx.BM_ERR_INVALID_ARG),
+    (dict(n_heads=6, n_kv_heads=4), bmx.BM_ERR_INVALID_ARG),
+    (dict(sm_scale=float("nan")), bmx.BM_ERR_INVALID_ARG),
+    (dict(sm_scale=-1.0), bmx.BM_ERR_INVALID_ARG),
+    (dict(head_dim=96), bmx.BM_ERR_UNSUPPORTED),
+    (dict(dtype=7), bmx.BM_ERR_UNSUPPORTED),
+    (dict(n_heads=16, n_kv_heads=2), bmx.BM_ERR_UNSUPPORTED),
+    (dict(n_heads=6, n_kv_heads=2), bmx.BM_ERR_UNSUPPORTED),
+    (dict(block=2048), bmx.BM_ERR_UNSUPPORTED),
+    (dict(kv_max=4000, block=512), bmx.BM_ERR_UNSUPPORTED),
+])
+def test_validate_dims_errors(kw, status):
+    assert status_of(bmx.bm_validate_dims, dims(**kw)) == status
+    assert bmx.bm_last_error() != ""
+
+
+def test_validate_dims_ok():
+    bmx.bm_validate_dims(dims())
+    bmx.bm_validate_dims(dims(dtype="f32", head_dim=64, n_heads=4, n_kv_heads=4))
+    assert bmx.bm_last_error() == ""
+
+
+def test_cache_pointer_checks():
+    d = dims()
+    for field in ("k", "v", "score", "pos", "len", "work"):
+        c = fake_cache(d)
+        setattr(c, field, 0)
+        assert status_of(bmx.bm_resume, d, c, 0, 0) == bmx.BM_ERR_INVALID_ARG
+    c = fake_cache(d)
+    c.k = FAKE + 8
+    assert status_of(bmx.bm_resume, d, c, 0, 0) == bmx.BM_ERR_INVALID_ARG
+    c = fake_cache(d)
+    c.work_bytes = 16
+    assert status_of(bmx.bm_resume, d, c, 0, 0) == bmx.BM_ERR_INVALID_ARG
+    c = fake_cache(d)
+    assert status_of(bmx.bm_resume, d, c, 200, 300) == bmx.BM_ERR_INVALID_ARG   # len > cap
+    assert status_of(bmx.bm_resume, d, c, 10, 5) == bmx.BM_ERR_INVALID_ARG      # len > next_pos
+
+
+def _ctx(d, length, next_pos):
+    return bmx.bm_resume(d, fake_cache(d), length, next_pos)
+
+
+def test_prefill_order_and_capacity_errors():
+    d = dims()
+    ctx = _ctx(d, 128, 192)
+    P = FAKE
+    try:
+        assert status_of(bmx.bm_prefill_block, ctx, 100, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
+        assert status_of(bmx.bm_prefill_block, ctx, 192, 0, P, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_prefill_block, ctx, 192, 65, P, P, P, P, 65, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_prefill_block, ctx, 192, 64, P, P, P, P, 32, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_prefill_block, ctx, 192, 64, 0, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_prefill_block, ctx, 192, 64, P + 2, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
+        assert bmx.bm_ctx_next_pos(ctx) == 192 and bmx.bm_ctx_len(ctx) == 128
+    finally:
+        bmx.bm_destroy(ctx)
+    # past the prompt
+    ctx = _ctx(d, 128, 480)
+    try:
+        assert status_of(bmx.bm_prefill_block, ctx, 480, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
+    finally:
+        bmx.bm_destroy(ctx)
+    # cache over the bound: must evict first
+    ctx = _ctx(d, 192, 192)
+    try:
+        assert status_of(bmx.bm_prefill_block, ctx, 192, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
+        assert status_of(bmx.bm_evict_compact, ctx, 190, 0) == bmx.BM_ERR_ORDER
+    finally:
+        bmx.bm_destroy(ctx)
+
+
+def test_evict_noop_when_within_bound():
+    d = dims()
+    ctx = _ctx(d, 100, 100)
+    try:
+        bmx.bm_evict_compact(ctx, 99, 0)          # nothing to cut: no device work
+        assert bmx.bm_ctx_len(ctx) == 100
+        assert status_of(bmx.bm_evict_compact, ctx, 98, 0) == bmx.BM_ERR_ORDER
+    finally:
+        bmx.bm_destroy(ctx)
+
+
+def test_decode_order_and_capacity_errors():
+    d = dims()
+    P = FAKE
+    ctx = _ctx(d, 128, 448)           # prefill not finished
+    try:
+        assert status_of(bmx.bm_decode_step, ctx, 448, P, P, P, P, 1, 0) == bmx.BM_ERR_ORDER
+    finally:
+        bmx.bm_destroy(ctx)
+    ctx = _ctx(d, 192, 512)           # last block not evicted
+    try:
+        assert status_of(bmx.bm_decode_step, ctx, 512, P, P, P, P, 1, 0) == bmx.BM_ERR_CAPACITY
+    finally:
+        bmx.bm_destroy(ctx)
+    ctx = _ctx(d, 128, 544)           # past s + max_gen
+    try:
+        assert status_of(bmx.bm_decode_step, ctx, 544, P, P, P, P, 1, 0) == bmx.BM_ERR_ORDER
+    finally:
+        bmx.bm_destroy(ctx)
+    ctx = _ctx(d, 128, 520)
+    try:
+        assert status_of(bmx.bm_decode_step, ctx, 519, P, P, P, P, 1, 0) == bmx.BM_ERR_ORDER
+        assert status_of(bmx.bm_decode_step, ctx, 520, P, P, P, P, 0, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_decode_step, ctx, 520, P, 0, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
+    finally:
+        bmx.bm_destroy(ctx)
+
+
+def test_null_context():
+    P = FAKE
+    assert status_of(bmx.bm_prefill_block, None, 0, 1, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_evict_compact, None, 0, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_decode_step, None, 0, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
+    assert bmx.bm_ctx_len(None) == -1 and bmx.bm_ctx_next_pos(None) == -1
+
+
+def test_algorithmic_work_figures():
+    # c2: b=64, GQA 32/8, d=128, s=4096, |kv|=512, block=256
+    f = bmx.prefill_flops(b=64, n_kv_heads=8, group=4, head_dim=128, s=4096, kv_max=512, block=256)
+    assert abs(f - 2.545e12) / 2.545e12 < 1e-3
+    by = bmx.decode_bytes_per_step(b=64, n_kv_heads=8, group=4, head_dim=128, kv_max=512,
+                                   elem_bytes=2)
+    assert by == 512 * 271368

@@ -48,6 +48,10 @@ class bm_cache(ctypes.Structure):
 
 
 def _load() -> ctypes.CDLL:
+    # torch ships its own HIP runtime under the same soname as ROCm's; load it
+    # first so this library binds to that single runtime instead of a second copy
+    import torch  # noqa: F401
+
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is not built; run `python -m paper_2412_05693_amd.build` "
@@ -178,7 +182,10 @@ class PDAttention:
                               dtype=dtype, sm_scale=sm_scale)
         bm_validate_dims(self.dims)
         self.tdtype = torch.float32 if self.dims.dtype == BM_F32 else torch.bfloat16
-        self.device = torch.device(device)
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
         self.cap = bm_cache_slots(self.dims)
         self.group = n_heads // n_kv_heads
         U = b * n_kv_heads

@@ -88,7 +88,7 @@ def test_bound_larger_than_prompt_then_decode_cuts():
     # decode appends without eviction until the bound is reached, then cuts one per step
     wl = C2.with_(b=1, s=300, kv_max=310, block=128, n_decode=20)
     st = _run(wl, synth.checked_units(wl, wl.units))
-    assert st.cuts == 300 + 20 - 310
+    assert st.cuts == wl.units * (300 + 20 - 310)
 
 
 def test_sharp_distribution():

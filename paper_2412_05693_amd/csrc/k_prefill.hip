@@ -18,11 +18,20 @@
 //   sweep 2 (S = Q K^T orientation: one key per lane) -- recompute the logits,
 //            P = exp2(z - m - log2 l) exactly, and sum over the rows held in
 //            the lane's registers, so each lane ends with one key's column sum.
-// Keys stream through LDS (double-buffered, one barrier per tile); V tiles are
-// stored as 8-key groups transposed to [group][d][8] so one 16-byte LDS read
-// yields an MFMA operand.  Keys of a 32-key sub-tile are stored in LDS row
-// order kappa (bits 2 and 3 of the row swapped), which makes the register
-// layout of the S^T accumulator coincide with the PV MFMA's B operand.
+// Both sweeps are software-pipelined: the MFMAs of tile t+1's logits are issued
+// before tile t's softmax, so the matrix cores and the VALU work overlap within
+// a wave.
+//
+// Key tiles hold 64 rows from one source: the unit's cache rows [0, len0) first,
+// then the block's input rows.  Tiles are copied global -> LDS by buffer loads
+// that write LDS directly (no staging registers); rows past a source's range
+// come back as zeros.  LDS rows are padded (the DMA writes zeros into the
+// padding slots), so the MFMA operand reads are free of bank conflicts and use
+// base + immediate addressing.
+// K rows of a 32-key sub-tile sit in LDS row order kappa (bits 2 and 3 of the
+// row swapped), which makes the register layout of the S^T accumulator equal
+// to the PV MFMA's B operand; V reaches the PV MFMA through gfx950's
+// transposing LDS load (ds_read_b64_tr_b16).
 #include <type_traits>
 
 #include "bm_internal.h"
@@ -35,9 +44,15 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __bf16 __attribute__((vector_size(8))) bf16v4;   // operand type of the LDS transpose read
+typedef __attribute__((address_space(3))) bf16v4 lds_bf16v4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kPosInf = __builtin_huge_valf();
+constexpr int kRsrcWord3 = 0x00020000;
+// s_waitcnt with vmcnt(0) and the other counters left alone
+constexpr int kWaitVm0 = 0x0F70;
 
 __device__ __forceinline__ int kappa(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
@@ -55,31 +70,25 @@ __device__ __forceinline__ int st_key(int st, int i, int j, int h) {
 }
 
 template <bool BF16, int D>
-struct Tile {
-  // LDS row strides in elements (16-byte padding)
-  static constexpr int kRow = BF16 ? D + 8 : D + 4;
-  static constexpr int kKElems = kKeyTile * kRow;
-  static constexpr int kGStride = D * 8 + 8;                    // bf16 V group stride
-  static constexpr int kVElems = BF16 ? 8 * kGStride : kKeyTile * kRow;
-  static constexpr int kQSteps = BF16 ? D / 16 : D / 2;         // MFMA K-steps over d
-  static constexpr int kMT = D / 32;                             // 32-row M-tiles of O^T
-  using elem_t = typename std::conditional<BF16, uint16_t, float>::type;
+struct Cfg {
+  using E = typename std::conditional<BF16, uint16_t, float>::type;
   using qfrag_t = typename std::conditional<BF16, bf16x8, float>::type;
-  static constexpr int kKChunks = kKeyTile * D * (int)sizeof(elem_t) / 16 / kThreads;
-  static constexpr int kVCombos = BF16 ? (8 * (D / 4) * 2) / kThreads : kKChunks;
+  static constexpr int RB = D * (int)sizeof(E);          // bytes per K/V row
+  static constexpr int CPR = RB / 16;                     // 16-byte chunks per row
+  // LDS rows are padded by one (K) or two (V) 16-byte chunks: the MFMA operand
+  // reads of K (16 lanes, 16 rows, one chunk each) and the transposing reads of
+  // V (4 rows x 32 bytes per 16-lane group) then fall in distinct banks.
+  static constexpr int KCP = CPR + 1, VCP = CPR + 2;     // chunks per padded row
+  static constexpr int KSTRIDE = KCP * 16, VSTRIDE = VCP * 16;
+  static constexpr int K_BYTES = kKeyTile * KSTRIDE, V_BYTES = kKeyTile * VSTRIDE;
+  static constexpr int QSTEPS = BF16 ? D / 16 : D / 2;   // MFMA K-steps over d
+  static constexpr int MT = D / 32;                       // 32-row M-tiles of O^T
 };
 
-template <bool BF16, int D>
-struct SMem {
-  using T = Tile<BF16, D>;
-  typename T::elem_t k[2][T::kKElems];
-  typename T::elem_t v[2][T::kVElems];
-  float cs[2][kWaves][kKeyTile];
-};
 
 template <bool BF16, int D>
-__device__ __forceinline__ f32x16 mfma_step(typename Tile<BF16, D>::qfrag_t a,
-                                            typename Tile<BF16, D>::qfrag_t b, f32x16 c) {
+__device__ __forceinline__ f32x16 mfma_step(typename Cfg<BF16, D>::qfrag_t a,
+                                            typename Cfg<BF16, D>::qfrag_t b, f32x16 c) {
   if constexpr (BF16) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   } else {
@@ -87,33 +96,41 @@ __device__ __forceinline__ f32x16 mfma_step(typename Tile<BF16, D>::qfrag_t a,
   }
 }
 
-// fragment of LDS row `row` of the K tile for K-step kk, lane half h
+// fragment of LDS row `row` of a K tile for K-step kk, lane half h
 template <bool BF16, int D>
-__device__ __forceinline__ typename Tile<BF16, D>::qfrag_t
-k_frag(const typename Tile<BF16, D>::elem_t* ks, int row, int h, int kk) {
-  using T = Tile<BF16, D>;
+__device__ __forceinline__ typename Cfg<BF16, D>::qfrag_t k_frag(const char* ks, int row, int h,
+                                                                 int kk) {
+  using C = Cfg<BF16, D>;
   if constexpr (BF16) {
-    const u32x4 w = *reinterpret_cast<const u32x4*>(ks + row * T::kRow + h * (D / 2) + 8 * kk);
-    return __builtin_bit_cast(bf16x8, w);
+    const int b = (h * (D / 2) + 8 * kk) * 2;
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + row * C::KSTRIDE + b));
   } else {
-    return ks[row * T::kRow + h * (D / 2) + kk];
+    const int b = (h * (D / 2) + kk) * 4;
+    return *reinterpret_cast<const float*>(ks + row * C::KSTRIDE + b);
   }
 }
 
 struct Geo {
   int u, bi, hk, pt, w, lane, n, h, g, sub;
   int pbase;       // first block position (relative to t0) of the workgroup
+  int wrow0;       // first query row (relative to t0) of this wave
   int row;         // this lane's query row (relative to t0) in S^T orientation
+  int wlast;       // last real query row of this wave
   bool qvalid;
   bool wave_active;
-  int nkeys_wg;    // keys the workgroup touches: len0 + its last position + 1
-  int nkeys_w;     // keys this wave's rows can see
+  int in_rows;     // block rows the workgroup reads: min(n_tok, pbase + PT)
+  int ntc, nt;     // cache tiles, all tiles
 };
 
 template <int G>
 __device__ __forceinline__ Geo make_geo(const PrefillArgs& a) {
   Geo s;
-  const int lin = blockIdx.x;
+  // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+  // L2).  Renumber them so that consecutive logical ids -- the workgroups of
+  // one unit -- land on the same XCD and share that unit's K/V in its L2.
+  const int nwg = gridDim.x, L = blockIdx.x;
+  const int q8 = nwg >> 3, r8 = nwg & 7, xcd = L & 7;
+  const int lin = xcd * q8 + min(xcd, r8) + (L >> 3);
   s.u = lin / a.npt_used;
   s.pt = lin - s.u * a.npt_used;
   s.bi = s.u / a.n_kv_heads;
@@ -126,142 +143,103 @@ __device__ __forceinline__ Geo make_geo(const PrefillArgs& a) {
   s.sub = s.w / G;
   constexpr int PT = kWaves * kRowsPerWave / G;
   s.pbase = s.pt * PT;
-  const int wrow0 = s.pbase + s.sub * kRowsPerWave;
-  s.row = wrow0 + s.n;
+  s.wrow0 = s.pbase + s.sub * kRowsPerWave;
+  s.row = s.wrow0 + s.n;
   s.qvalid = s.row < a.n_tok;
-  s.wave_active = wrow0 < a.n_tok;
-  s.nkeys_wg = a.len0 + min(a.n_tok, s.pbase + PT);
-  s.nkeys_w = a.len0 + min(a.n_tok, wrow0 + kRowsPerWave);
+  s.wave_active = s.wrow0 < a.n_tok;
+  s.wlast = min(a.n_tok - 1, s.wrow0 + kRowsPerWave - 1);
+  s.in_rows = min(a.n_tok, s.pbase + PT);
+  s.ntc = (a.len0 + kKeyTile - 1) / kKeyTile;
+  s.nt = s.ntc + (s.in_rows + kKeyTile - 1) / kKeyTile;
   return s;
 }
 
-// ---------------------------------------------------------------------------
-// staging: global -> registers -> LDS
-// ---------------------------------------------------------------------------
-template <bool BF16, int D>
-struct Stage {
-  using T = Tile<BF16, D>;
-  using E = typename T::elem_t;
-  u32x4 kr[T::kKChunks];
-  u32x2 vr[BF16 ? T::kVCombos * 4 : 1];
-  u32x4 vf[BF16 ? 1 : T::kKChunks];
-
-  __device__ __forceinline__ static const E* key_src(const PrefillArgs& a, const Geo& s,
-                                                    const E* kc, const E* kin, int key) {
-    if (key < a.len0) return kc + ((int64_t)s.u * a.cap + key) * D;
-    if (key < s.nkeys_wg)
-      return kin + (((int64_t)s.bi * a.n_kv_heads + s.hk) * a.seq_ld + (key - a.len0)) * D;
-    return nullptr;
-  }
-
-  __device__ __forceinline__ void load_k(const PrefillArgs& a, const Geo& s, int tile_base) {
-    const E* kc = static_cast<const E*>(a.kc);
-    const E* kin = static_cast<const E*>(a.kin);
-    constexpr int CPR = D * (int)sizeof(E) / 16;  // 16-byte chunks per row
-#pragma unroll
-    for (int i = 0; i < T::kKChunks; ++i) {
-      const int c = threadIdx.x + kThreads * i;
-      const int r = c / CPR, cc = c - r * CPR;
-      const int key = tile_base + (r & ~31) + kappa(r & 31);
-      const E* src = key_src(a, s, kc, kin, key);
-      kr[i] = src ? *reinterpret_cast<const u32x4*>(src + cc * (16 / sizeof(E))) : u32x4{0, 0, 0, 0};
-    }
-  }
-  __device__ __forceinline__ void store_k(E* ks) const {
-    constexpr int CPR = D * (int)sizeof(E) / 16;
-#pragma unroll
-    for (int i = 0; i < T::kKChunks; ++i) {
-      const int c = threadIdx.x + kThreads * i;
-      const int r = c / CPR, cc = c - r * CPR;
-      *reinterpret_cast<u32x4*>(ks + r * T::kRow + cc * (16 / sizeof(E))) = kr[i];
-    }
-  }
-
-  __device__ __forceinline__ void load_v(const PrefillArgs& a, const Geo& s, int tile_base) {
-    const E* vc = static_cast<const E*>(a.vc);
-    const E* vin = static_cast<const E*>(a.vin);
-    if constexpr (BF16) {
-      // combo = (group of 8 keys, half of the group, 4 consecutive d)
-#pragma unroll
-      for (int i = 0; i < T::kVCombos; ++i) {
-        const int c = threadIdx.x + kThreads * i;
-        const int dq = c % (D / 4);
-        const int rest = c / (D / 4);
-        const int kh = rest & 1, grp = rest >> 1;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = tile_base + 8 * grp + 4 * kh + e;
-          const E* src = key_src(a, s, vc, vin, key);
-          vr[4 * i + e] = src ? *reinterpret_cast<const u32x2*>(src + 4 * dq) : u32x2{0, 0};
-        }
-      }
-    } else {
-      constexpr int CPR = D * 4 / 16;
-#pragma unroll
-      for (int i = 0; i < T::kKChunks; ++i) {
-        const int c = threadIdx.x + kThreads * i;
-        const int r = c / CPR, cc = c - r * CPR;
-        const E* src = key_src(a, s, vc, vin, tile_base + r);
-        vf[i] = src ? *reinterpret_cast<const u32x4*>(src + cc * 4) : u32x4{0, 0, 0, 0};
-      }
-    }
-  }
-  __device__ __forceinline__ void store_v(E* vs) const {
-    if constexpr (BF16) {
-#pragma unroll
-      for (int i = 0; i < T::kVCombos; ++i) {
-        const int c = threadIdx.x + kThreads * i;
-        const int dq = c % (D / 4);
-        const int rest = c / (D / 4);
-        const int kh = rest & 1, grp = rest >> 1;
-        const u32x2 r0 = vr[4 * i + 0], r1 = vr[4 * i + 1], r2 = vr[4 * i + 2], r3 = vr[4 * i + 3];
-        // transpose 4 keys x 4 d (bf16) into 4 d-rows of 4 keys
-        u32x2 o0, o1, o2, o3;
-        o0.x = (r0.x & 0xffffu) | (r1.x << 16);
-        o0.y = (r2.x & 0xffffu) | (r3.x << 16);
-        o1.x = (r0.x >> 16) | (r1.x & 0xffff0000u);
-        o1.y = (r2.x >> 16) | (r3.x & 0xffff0000u);
-        o2.x = (r0.y & 0xffffu) | (r1.y << 16);
-        o2.y = (r2.y & 0xffffu) | (r3.y << 16);
-        o3.x = (r0.y >> 16) | (r1.y & 0xffff0000u);
-        o3.y = (r2.y >> 16) | (r3.y & 0xffff0000u);
-        E* base = vs + grp * T::kGStride + (4 * dq) * 8 + 4 * kh;
-        *reinterpret_cast<u32x2*>(base + 0 * 8) = o0;
-        *reinterpret_cast<u32x2*>(base + 1 * 8) = o1;
-        *reinterpret_cast<u32x2*>(base + 2 * 8) = o2;
-        *reinterpret_cast<u32x2*>(base + 3 * 8) = o3;
-      }
-    } else {
-      constexpr int CPR = D * 4 / 16;
-#pragma unroll
-      for (int i = 0; i < T::kKChunks; ++i) {
-        const int c = threadIdx.x + kThreads * i;
-        const int r = c / CPR, cc = c - r * CPR;
-        *reinterpret_cast<u32x4*>(vs + r * T::kRow + cc * 4) = vf[i];
-      }
-    }
-  }
+// Where tile t comes from and which of its rows exist.
+struct TileInfo {
+  bool cache;      // rows from the unit's cache (else the block's input rows)
+  int base;        // first source row of the tile
+  int slot0;       // cache slot of the tile's row 0 (for the score sums)
+  int valid;       // rows of the tile that exist
 };
+
+__device__ __forceinline__ TileInfo tile_info(const PrefillArgs& a, const Geo& s, int t) {
+  TileInfo ti;
+  ti.cache = t < s.ntc;
+  ti.base = (ti.cache ? t : t - s.ntc) * kKeyTile;
+  ti.slot0 = ti.cache ? ti.base : a.len0 + ti.base;
+  ti.valid = min(kKeyTile, (ti.cache ? a.len0 : s.in_rows) - ti.base);
+  return ti;
+}
+
+// does the wave see any key of tile t; does the tile need masking for it
+__device__ __forceinline__ bool tile_active(const Geo& s, const TileInfo& ti) {
+  return s.wave_active && (ti.cache || ti.base <= s.wlast);
+}
+__device__ __forceinline__ bool tile_masked(const Geo& s, const TileInfo& ti) {
+  return ti.cache ? ti.valid < kKeyTile : ti.base + kKeyTile - 1 > s.wrow0;
+}
+
+// Tiles of K (rows in kappa order) and V are copied into LDS with buffer loads
+// that write LDS directly; lane i of instruction j of wave w fills the 16-byte
+// chunk (w * DMA_PER_WAVE + j) * 64 + i of the tile.
+struct Rows {
+  __amdgpu_buffer_rsrc_t cache;   // the unit's cache rows [0, len0)
+  __amdgpu_buffer_rsrc_t input;   // the block's rows this workgroup reads
+};
+
+// An out-of-range offset: the lane writes zeros (used for the padding slots).
+constexpr int kOutOfRange = 0x7FFFFFF0;
+
+// Copy one tile into padded LDS rows.  Slot g = 64 * seg + lane of the tile
+// holds chunk g % CP of row g / CP; chunks >= CPR are padding.  K rows are
+// stored in kappa order within each 32-row sub-tile.
+template <bool BF16, int D, bool K>
+__device__ __forceinline__ void dma_rows(char* dst, const Rows& rows, const TileInfo& ti,
+                                         const Geo& s) {
+  using C = Cfg<BF16, D>;
+  constexpr int CP = K ? C::KCP : C::VCP;   // also the number of 1 KB segments
+#pragma unroll
+  for (int j = 0; j < (CP + kWaves - 1) / kWaves; ++j) {
+    const int seg = s.w + kWaves * j;
+    if (seg < CP) {   // uniform per wave
+      const int g = seg * 64 + s.lane;
+      const int r = g / CP, c = g - r * CP;
+      const int key = K ? (r & ~31) + kappa(r & 31) : r;
+      const int off = c < C::CPR ? (ti.base + key) * C::RB + c * 16 : kOutOfRange;
+      if (ti.cache)   // uniform: one source per tile
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rows.cache, (lds_void*)(dst + seg * 1024), 16, off, 0, 0, 0);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rows.input, (lds_void*)(dst + seg * 1024), 16, off, 0, 0, 0);
+    }
+  }
+}
 
 template <bool BF16, int D, int G>
 __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_attn_kernel(PrefillArgs a) {
-  using T = Tile<BF16, D>;
-  using E = typename T::elem_t;
-  __shared__ SMem<BF16, D> sm;
+  using C = Cfg<BF16, D>;
+  using E = typename C::E;
+  constexpr int RB = C::RB;
+  // separate arrays per buffer: with the ping-pong index known at compile time
+  // the compiler can tell the tile being filled from the tile being read
+  __shared__ __attribute__((aligned(1024))) char kb0[C::K_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kb1[C::K_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vb0[C::V_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vb1[C::V_BYTES];
+  __shared__ float cs0[kWaves][kKeyTile];
+  __shared__ float cs1[kWaves][kKeyTile];
   const Geo s = make_geo<G>(a);
   const int tid = threadIdx.x;
 
   // ---- append the workgroup's block rows to the cache tail (Sec. 3.2: new
   //      entries start with score 0; the score is written by score_reduce) ----
+  const int64_t plane = ((int64_t)s.bi * a.n_kv_heads + s.hk) * a.seq_ld;
   {
-    constexpr int PT = kWaves * kRowsPerWave / G;
-    constexpr int CPR = D * (int)sizeof(E) / 16;
-    const int r0 = s.pbase, r1 = min(a.n_tok, s.pbase + PT);
+    constexpr int CPR = C::CPR;
+    const int r0 = s.pbase, r1 = s.in_rows;
     const E* kin = static_cast<const E*>(a.kin);
     const E* vin = static_cast<const E*>(a.vin);
     E* kc = static_cast<E*>(a.kc);
     E* vc = static_cast<E*>(a.vc);
-    const int64_t plane = ((int64_t)s.bi * a.n_kv_heads + s.hk) * a.seq_ld;
     for (int c = tid; c < (r1 - r0) * CPR; c += kThreads) {
       const int r = r0 + c / CPR, cc = c % CPR;
       const int64_t dst = ((int64_t)s.u * a.cap + a.len0 + r) * D + cc * (16 / sizeof(E));
@@ -273,14 +251,25 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       a.pos[(int64_t)s.u * a.cap + a.len0 + r] = a.t0 + r;
   }
 
+  // ---- row sources as buffer resources (out-of-range rows read as zero) ----
+  Rows krows, vrows;
+  krows.cache = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<E*>(static_cast<const E*>(a.kc)) + (int64_t)s.u * a.cap * D, 0, a.len0 * RB, kRsrcWord3);
+  krows.input = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<E*>(static_cast<const E*>(a.kin)) + plane * D, 0, s.in_rows * RB, kRsrcWord3);
+  vrows.cache = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<E*>(static_cast<const E*>(a.vc)) + (int64_t)s.u * a.cap * D, 0, a.len0 * RB, kRsrcWord3);
+  vrows.input = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<E*>(static_cast<const E*>(a.vin)) + plane * D, 0, s.in_rows * RB, kRsrcWord3);
+
   // ---- query fragments: lane (n, h) holds row n, d-range [h*D/2, (h+1)*D/2) ----
-  typename T::qfrag_t qf[T::kQSteps];
+  typename C::qfrag_t qf[C::QSTEPS];
   {
     const int qh = s.hk * G + s.g;
     const E* q = static_cast<const E*>(a.q) +
                  (((int64_t)s.bi * a.n_heads + qh) * a.seq_ld + s.row) * D + s.h * (D / 2);
 #pragma unroll
-    for (int kk = 0; kk < T::kQSteps; ++kk) {
+    for (int kk = 0; kk < C::QSTEPS; ++kk) {
       if constexpr (BF16) {
         const u32x4 w = s.qvalid ? *reinterpret_cast<const u32x4*>(q + 8 * kk) : u32x4{0, 0, 0, 0};
         qf[kk] = __builtin_bit_cast(bf16x8, w);
@@ -290,110 +279,157 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     }
   }
 
-  const int ntiles = (s.nkeys_wg + kKeyTile - 1) / kKeyTile;
+  const int nt = s.nt;
   const float c2 = a.scale_log2;
-  // a row sees key slots j <= lim (cached slots, then block keys up to itself)
-  const int lim = a.len0 + (s.qvalid ? s.row : a.n_tok - 1);
+  // the row this lane's causal mask uses (padding rows reuse the last real row)
+  const int qrow = s.qvalid ? s.row : a.n_tok - 1;
+
+  // logits of one tile: S^T (one query per lane) or S (one key per lane)
+  auto qk_st = [&](const char* ks, f32x16* acc) __device__ {
+    acc[0] = f32x16{};
+    acc[1] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < C::QSTEPS; ++kk) {
+      acc[0] = mfma_step<BF16, D>(k_frag<BF16, D>(ks, s.n, s.h, kk), qf[kk], acc[0]);
+      acc[1] = mfma_step<BF16, D>(k_frag<BF16, D>(ks, 32 + s.n, s.h, kk), qf[kk], acc[1]);
+    }
+  };
+  auto qk_s = [&](const char* ks, f32x16* acc) __device__ {
+    acc[0] = f32x16{};
+    acc[1] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < C::QSTEPS; ++kk) {
+      acc[0] = mfma_step<BF16, D>(qf[kk], k_frag<BF16, D>(ks, s.n, s.h, kk), acc[0]);
+      acc[1] = mfma_step<BF16, D>(qf[kk], k_frag<BF16, D>(ks, 32 + s.n, s.h, kk), acc[1]);
+    }
+  };
 
   // ======================= sweep 1: online softmax + PV =======================
-  f32x16 oacc[T::kMT];
+  f32x16 oacc[C::MT];
 #pragma unroll
-  for (int mt = 0; mt < T::kMT; ++mt) oacc[mt] = f32x16{};
+  for (int mt = 0; mt < C::MT; ++mt) oacc[mt] = f32x16{};
   float m_run = kNegInf, l_run = 0.0f;
 
-  Stage<BF16, D> stg;
-  stg.load_k(a, s, 0);
-  stg.load_v(a, s, 0);
-  stg.store_k(sm.k[0]);
-  stg.store_v(sm.v[0]);
-  __syncthreads();
+  // softmax of tile t (S^T in sacc) and O^T += V^T P^T
+  auto sweep1_tile = [&](auto mask_tag, f32x16* sacc, const char* vs, const TileInfo& ti) __device__ {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    if constexpr (MASK) {
+      // key k of the tile is visible iff k <= lim_k
+      const int lim_k = ti.cache ? ti.valid - 1 : qrow - ti.base;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          sacc[st][r] = st_key(st, r >> 2, r & 3, s.h) <= lim_k ? sacc[st][r] : kNegInf;
+    }
+    // tile max on the raw logits (the scale is positive), then one fma per exp2
+    float tmax = kNegInf;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[st][r]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float m_new = fmaxf(m_run, tmax * c2);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    float psum = 0.0f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][r], c2, -m_new));
+        sacc[st][r] = p;
+        psum += p;
+      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    if (__ballot(alpha != 1.0f) != 0) {
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[mt][r] *= alpha;
+    }
+    if constexpr (BF16) {
+      // A operand (V^T): lane (n, h) needs V[key][32 mt + n] for the 8 keys
+      // 16 ks + 8 h + e of P's k-slots.  The LDS transpose load gives lane i of
+      // a 16-lane group column i of the 4 x 16 block formed by the group's
+      // lanes 4r..4r+3 (row r), so lane 4r + c points at V[key0 + r][d0 + 4c]
+      // and receives V[key0 + 0..3][d0 + i].
+      const int j16 = s.lane & 15, dhalf = (s.lane >> 4) & 1;
+      const int vrow = 8 * s.h + (j16 >> 2);
+      const int vb = (16 * dhalf + 4 * (j16 & 3)) * 2;
+#pragma unroll
+      for (int ks4 = 0; ks4 < 4; ++ks4) {
+        const int st = ks4 >> 1, half = ks4 & 1;
+        u32x4 pw;
+        pw.x = pack_bf16x2(sacc[st][8 * half + 0], sacc[st][8 * half + 1]);
+        pw.y = pack_bf16x2(sacc[st][8 * half + 2], sacc[st][8 * half + 3]);
+        pw.z = pack_bf16x2(sacc[st][8 * half + 4], sacc[st][8 * half + 5]);
+        pw.w = pack_bf16x2(sacc[st][8 * half + 6], sacc[st][8 * half + 7]);
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
+          const int r0 = 16 * ks4 + vrow, b = vb + 64 * mt;
+          const bf16v4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4*)(vs + r0 * C::VSTRIDE + b));
+          const bf16v4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4*)(vs + (r0 + 4) * C::VSTRIDE + b));
+          const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+          const u32x4 vw = {l2.x, l2.y, h2.x, h2.y};
+          oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb,
+                                                              oacc[mt], 0, 0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = st_key(st, r >> 2, r & 3, s.h);
+#pragma unroll
+          for (int mt = 0; mt < C::MT; ++mt) {
+            const float vv = *reinterpret_cast<const float*>(vs + key * C::VSTRIDE + (32 * mt + s.n) * 4);
+            oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x2f32(vv, sacc[st][r], oacc[mt], 0, 0, 0);
+          }
+        }
+    }
+  };
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int tile_base = t * kKeyTile;
-    if (t + 1 < ntiles) {
-      stg.load_k(a, s, tile_base + kKeyTile);
-      stg.load_v(a, s, tile_base + kKeyTile);
+  // prologue: K(0), V(0), K(1) land in LDS; logits of tile 0
+  dma_rows<BF16, D, true>(kb0, krows, tile_info(a, s, 0), s);
+  dma_rows<BF16, D, false>(vb0, vrows, tile_info(a, s, 0), s);
+  if (nt > 1) dma_rows<BF16, D, true>(kb1, krows, tile_info(a, s, 1), s);
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+  // logits ping-pong between two register sets; the loop is unrolled by two so
+  // every buffer choice below is a compile-time constant
+  f32x16 sa[2], sb[2];
+  if (tile_active(s, tile_info(a, s, 0))) qk_st(kb0, sa);
+  __syncthreads();   // every wave has read K(0) before iteration 0 refills its buffer
+  // iteration t (parity P = t & 1): K(t+1) and V(t) are in LDS and `cur` holds
+  // tile t's logits; K(t+2) and V(t+1) are fetched meanwhile
+  auto sweep1_iter = [&](auto par, int t, f32x16* cur, f32x16* nxt) __device__ {
+    constexpr int P = decltype(par)::value;
+    char* k_fill = P == 0 ? kb0 : kb1;
+    char* k_next = P == 0 ? kb1 : kb0;
+    char* v_cur = P == 0 ? vb0 : vb1;
+    char* v_fill = P == 0 ? vb1 : vb0;
+    const TileInfo ti = tile_info(a, s, t);
+    if (t + 2 < nt) dma_rows<BF16, D, true>(k_fill, krows, tile_info(a, s, t + 2), s);
+    if (t + 1 < nt) {
+      const TileInfo tn = tile_info(a, s, t + 1);
+      dma_rows<BF16, D, false>(v_fill, vrows, tn, s);
+      if (tile_active(s, tn)) qk_st(k_next, nxt);
     }
-    if (s.wave_active && tile_base < s.nkeys_w) {
-      const E* ks = sm.k[buf];
-      const E* vs = sm.v[buf];
-      f32x16 sacc[2];
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        sacc[st] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < T::kQSteps; ++kk)
-          sacc[st] = mfma_step<BF16, D>(k_frag<BF16, D>(ks, st * 32 + s.n, s.h, kk), qf[kk], sacc[st]);
-      }
-      // mask, scale, tile max
-      float tmax = kNegInf;
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = tile_base + st_key(st, r >> 2, r & 3, s.h);
-          const float x = key <= lim ? sacc[st][r] * c2 : kNegInf;
-          sacc[st][r] = x;
-          tmax = fmaxf(tmax, x);
-        }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float m_new = fmaxf(m_run, tmax);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      float psum = 0.0f;
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(sacc[st][r] - m_new);
-          sacc[st][r] = p;
-          psum += p;
-        }
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
-      if (__ballot(alpha != 1.0f) != 0) {
-#pragma unroll
-        for (int mt = 0; mt < T::kMT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[mt][r] *= alpha;
-      }
-      // O^T += V^T P^T
-      if constexpr (BF16) {
-#pragma unroll
-        for (int ks4 = 0; ks4 < 4; ++ks4) {
-          const int st = ks4 >> 1, half = ks4 & 1;
-          u32x4 pw;
-          pw.x = pack_bf16x2(sacc[st][8 * half + 0], sacc[st][8 * half + 1]);
-          pw.y = pack_bf16x2(sacc[st][8 * half + 2], sacc[st][8 * half + 3]);
-          pw.z = pack_bf16x2(sacc[st][8 * half + 4], sacc[st][8 * half + 5]);
-          pw.w = pack_bf16x2(sacc[st][8 * half + 6], sacc[st][8 * half + 7]);
-          const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-          const E* vg = vs + (2 * ks4 + s.h) * T::kGStride;
-#pragma unroll
-          for (int mt = 0; mt < T::kMT; ++mt) {
-            const u32x4 vw = *reinterpret_cast<const u32x4*>(vg + (32 * mt + s.n) * 8);
-            oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb,
-                                                                oacc[mt], 0, 0, 0);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = st_key(st, r >> 2, r & 3, s.h);
-#pragma unroll
-            for (int mt = 0; mt < T::kMT; ++mt)
-              oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x2f32(vs[key * T::kRow + 32 * mt + s.n],
-                                                              sacc[st][r], oacc[mt], 0, 0, 0);
-          }
-      }
+    if (tile_active(s, ti)) {
+      if (tile_masked(s, ti))
+        sweep1_tile(std::true_type{}, cur, v_cur, ti);
+      else
+        sweep1_tile(std::false_type{}, cur, v_cur, ti);
     }
-    if (t + 1 < ntiles) {
-      stg.store_k(sm.k[buf ^ 1]);
-      stg.store_v(sm.v[buf ^ 1]);
-    }
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
+  };
+  for (int t = 0; t < nt; t += 2) {
+    sweep1_iter(std::integral_constant<int, 0>{}, t, sa, sb);
+    if (t + 1 < nt) sweep1_iter(std::integral_constant<int, 1>{}, t + 1, sb, sa);
   }
 
   // ---- finish rows: normalise, store O, row log-sum-exp (log2 units) ----
@@ -406,7 +442,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       const int qh = s.hk * G + s.g;
       E* o = static_cast<E*>(a.o) + (((int64_t)s.bi * a.n_heads + qh) * a.seq_ld + s.row) * D;
 #pragma unroll
-      for (int mt = 0; mt < T::kMT; ++mt)
+      for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int d0 = 32 * mt + 8 * i + 4 * s.h;
@@ -426,52 +462,71 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   // S orientation: lane (n, h) holds key n of a 32-key sub-tile and rows
   // 8i + 4h + j of the wave's 32 rows in accumulator register 4i + j.
   float lse_r[16];
-  int lim_r[16];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int rr = 8 * (r >> 2) + 4 * s.h + (r & 3);
-    lse_r[r] = __shfl(lse2, rr);
-    lim_r[r] = a.len0 + s.pbase + s.sub * kRowsPerWave + rr;
-  }
+  for (int r = 0; r < 16; ++r) lse_r[r] = __shfl(lse2, 8 * (r >> 2) + 4 * s.h + (r & 3));
   float* partial = a.partial + ((int64_t)s.u * a.npt_stride + s.pt) * a.cap;
 
-  stg.load_k(a, s, 0);
-  stg.store_k(sm.k[0]);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int tile_base = t * kKeyTile;
-    if (t + 1 < ntiles) stg.load_k(a, s, tile_base + kKeyTile);
-    if (s.wave_active && tile_base < s.nkeys_w) {
-      const E* ks = sm.k[buf];
+  auto sweep2_tile = [&](auto mask_tag, f32x16* acc, const TileInfo& ti, float (*cs)[kKeyTile]) __device__ {
+    constexpr bool MASK = decltype(mask_tag)::value;
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        f32x16 acc = f32x16{};
+    for (int st = 0; st < 2; ++st) {
+      const int key = 32 * st + kappa(s.n);
+      float csum = 0.0f;
 #pragma unroll
-        for (int kk = 0; kk < T::kQSteps; ++kk)
-          acc = mfma_step<BF16, D>(qf[kk], k_frag<BF16, D>(ks, st * 32 + s.n, s.h, kk), acc);
-        const int key = tile_base + 32 * st + kappa(s.n);
-        float csum = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float x = key <= lim_r[r] ? acc[r] * c2 - lse_r[r] : kNegInf;
-          csum += __builtin_amdgcn_exp2f(x);
+      for (int r = 0; r < 16; ++r) {
+        float x = fmaf(acc[st][r], c2, -lse_r[r]);
+        if constexpr (MASK) {
+          const int qr = s.wrow0 + 8 * (r >> 2) + 4 * s.h + (r & 3);
+          const int lim_k = ti.cache ? ti.valid - 1 : qr - ti.base;
+          x = key <= lim_k ? x : kNegInf;
         }
-        csum += __shfl_xor(csum, 32);
-        if (s.h == 0) sm.cs[buf][s.w][32 * st + kappa(s.n)] = csum;
+        csum += __builtin_amdgcn_exp2f(x);
       }
-    } else if (s.lane < 32) {
-      sm.cs[buf][s.w][s.lane] = 0.0f;
-      sm.cs[buf][s.w][32 + s.lane] = 0.0f;
+      csum += __shfl_xor(csum, 32);
+      if (s.h == 0) cs[s.w][key] = csum;
     }
-    if (t + 1 < ntiles) stg.store_k(sm.k[buf ^ 1]);
+  };
+
+  // prologue: K(0), K(1) land in LDS; logits of tile 0
+  dma_rows<BF16, D, true>(kb0, krows, tile_info(a, s, 0), s);
+  if (nt > 1) dma_rows<BF16, D, true>(kb1, krows, tile_info(a, s, 1), s);
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+  if (tile_active(s, tile_info(a, s, 0))) qk_s(kb0, sa);
+  __syncthreads();   // every wave has read K(0) before iteration 0 refills its buffer
+  // iteration t (parity P = t & 1): K(t+1) is in LDS and `cur` holds tile t's logits
+  auto sweep2_iter = [&](auto par, int t, f32x16* cur, f32x16* nxt) __device__ {
+    constexpr int P = decltype(par)::value;
+    char* k_fill = P == 0 ? kb0 : kb1;
+    char* k_next = P == 0 ? kb1 : kb0;
+    float (*cs)[kKeyTile] = P == 0 ? cs0 : cs1;
+    const TileInfo ti = tile_info(a, s, t);
+    if (t + 2 < nt) dma_rows<BF16, D, true>(k_fill, krows, tile_info(a, s, t + 2), s);
+    if (t + 1 < nt) {
+      const TileInfo tn = tile_info(a, s, t + 1);
+      if (tile_active(s, tn)) qk_s(k_next, nxt);
+    }
+    if (tile_active(s, ti)) {
+      if (tile_masked(s, ti))
+        sweep2_tile(std::true_type{}, cur, ti, cs);
+      else
+        sweep2_tile(std::false_type{}, cur, ti, cs);
+    } else if (s.lane < 32) {
+      cs[s.w][s.lane] = 0.0f;
+      cs[s.w][32 + s.lane] = 0.0f;
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
-    if (tid < kKeyTile && tile_base + tid < s.nkeys_wg) {
+    if (tid < ti.valid) {
       float acc = 0.0f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) acc += sm.cs[buf][w][tid];
-      partial[tile_base + tid] = acc;
+      for (int w = 0; w < kWaves; ++w) acc += cs[w][tid];
+      partial[ti.slot0 + tid] = acc;
     }
+  };
+  for (int t = 0; t < nt; t += 2) {
+    sweep2_iter(std::integral_constant<int, 0>{}, t, sa, sb);
+    if (t + 1 < nt) sweep2_iter(std::integral_constant<int, 1>{}, t + 1, sb, sa);
   }
 }
 

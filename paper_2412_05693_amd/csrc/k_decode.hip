@@ -56,8 +56,9 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   const int L = len0 + 1;
   const int Lp = (L + 3) & ~3;
   float* P = dsm;                 // [G][Lp] logits, then probabilities
-  float* sc = P + G * Lp;         // [Lp] updated scores
+  float* sc = P + G * Lp;         // [Lp] scores (prefetched, then updated)
   float* red = sc + Lp;           // [4][G][D] partial outputs per wave
+  int32_t* pos_s = reinterpret_cast<int32_t*>(red + 4 * G * D);   // [Lp] positions
 
   const E* kc = static_cast<const E*>(a.kc) + (int64_t)u * a.cap * D;
   const E* vc = static_cast<const E*>(a.vc) + (int64_t)u * a.cap * D;
@@ -66,6 +67,16 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   const E* vnew = static_cast<const E*>(a.vin) + plane * D;
   const E* qbase = static_cast<const E*>(a.q) + ((int64_t)bi * a.n_heads + hk * G) * a.seq_ld * D;
   const float c2 = a.scale_log2;
+
+  // prefetch the scores and positions (used after the softmax) into LDS
+  {
+    const float* score = a.score + (int64_t)u * a.cap;
+    const int32_t* pos = a.pos + (int64_t)u * a.cap;
+    for (int j = tid; j < L; j += 256) {
+      sc[j] = j < len0 ? score[j] : 0.0f;
+      pos_s[j] = j < len0 ? pos[j] : a.cur_pos;
+    }
+  }
 
   // ---------------- 1. logits ----------------
   if constexpr (BF16) {
@@ -126,6 +137,18 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
+  // first batch of V rows for phase 4, in flight during the softmax
+  constexpr int NKL4 = 256 / CPR;
+  constexpr int UNR = 4;
+  const int c4 = tid % CPR, kl4 = tid / CPR;
+  u32x4 vw[UNR];
+#pragma unroll
+  for (int r = 0; r < UNR; ++r) {
+    const int j = kl4 + r * NKL4;
+    const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
+    vw[r] = src ? *reinterpret_cast<const u32x4*>(src + c4 * EPC) : u32x4{0, 0, 0, 0};
+  }
+
   // ---------------- 2. softmax per query head ----------------
   for (int g = w; g < G; g += 4) {
     float* pg = P + g * Lp;
@@ -149,18 +172,15 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   // ---------------- 3. scores and ranking ----------------
   const bool evict = L > a.kv_max;
   {
-    const float* score = a.score + (int64_t)u * a.cap;
-    const int32_t* pos = a.pos + (int64_t)u * a.cap;
     uint64_t best = ~0ull;
     int bslot = -1;
     for (int j = tid; j < L; j += 256) {
       float ps = 0.0f;
 #pragma unroll
       for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
-      const float s = (j < len0 ? score[j] : 0.0f) + ps;
+      const float s = sc[j] + ps;
       sc[j] = s;
-      const int pj = j < len0 ? pos[j] : a.cur_pos;
-      const uint64_t key = rank_key(s, pj, a.cur_pos);
+      const uint64_t key = rank_key(s, pos_s[j], a.cur_pos);
       if (key < best) {
         best = key;
         bslot = j;
@@ -183,21 +203,21 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 
   // ---------------- 4. outputs o_g = sum_j P[g][j] v_j ----------------
   {
-    constexpr int NKL = 256 / CPR;
-    constexpr int UNR = 4;
-    const int c = tid % CPR, kl = tid / CPR;
+    constexpr int NKL = NKL4;
+    const int c = c4;
     float acc[G][EPC];
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int e = 0; e < EPC; ++e) acc[g][e] = 0.0f;
-    for (int j0 = kl; j0 < L; j0 += NKL * UNR) {
-      u32x4 vw[UNR];
+    for (int j0 = kl4; j0 < L; j0 += NKL * UNR) {
+      // next batch in flight while this one is consumed
+      u32x4 vn[UNR];
 #pragma unroll
       for (int r = 0; r < UNR; ++r) {
-        const int j = j0 + r * NKL;
+        const int j = j0 + (UNR + r) * NKL;
         const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
-        vw[r] = src ? *reinterpret_cast<const u32x4*>(src + c * EPC) : u32x4{0, 0, 0, 0};
+        vn[r] = src ? *reinterpret_cast<const u32x4*>(src + c * EPC) : u32x4{0, 0, 0, 0};
       }
 #pragma unroll
       for (int r = 0; r < UNR; ++r) {
@@ -221,6 +241,8 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
           for (int e = 0; e < EPC; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
         }
       }
+#pragma unroll
+      for (int r = 0; r < UNR; ++r) vw[r] = vn[r];
     }
     // reduce the lanes of a wave that share chunk c, then across waves in LDS
 #pragma unroll
@@ -287,7 +309,7 @@ template <bool BF16, int D, int G>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   const int L = a.len0 + 1;
   const int Lp = (L + 3) & ~3;
-  const size_t lds = sizeof(float) * ((size_t)G * Lp + Lp + 4 * G * D);
+  const size_t lds = sizeof(float) * ((size_t)G * Lp + Lp + 4 * G * D + Lp);
   hipLaunchKernelGGL((decode_kernel<BF16, D, G>), dim3((unsigned)a.units), dim3(256), lds, stream,
                      a);
   return hipGetLastError();

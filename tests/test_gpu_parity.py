@@ -194,3 +194,16 @@ def test_snapshot_resume_bit_exact():
     torch.cuda.synchronize()
     assert torch.equal(o2, o)
     assert torch.equal(pd2.score, pd.score) and torch.equal(pd2.pos, pd.pos)
+
+
+def test_c3_full_shape_sampled_units():
+    wl = synth.WORKLOADS["c3"]
+    st = _run(wl, synth.checked_units(wl, 6))
+    assert st.cuts > 0
+
+
+def test_c4_full_shape_sampled_units():
+    # decode-heavy: 512 steps with one eviction each per unit
+    wl = synth.WORKLOADS["c4"]
+    st = _run(wl, synth.checked_units(wl, 6))
+    assert st.cuts > 0

@@ -51,6 +51,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kPosInf = __builtin_huge_valf();
 constexpr int kRsrcWord3 = 0x00020000;
+constexpr float kRescaleLog2 = 8.0f;
 // s_waitcnt with vmcnt(0) and the other counters left alone
 constexpr int kWaitVm0 = 0x0F70;
 
@@ -181,10 +182,12 @@ __device__ __forceinline__ bool tile_masked(const Geo& s, const TileInfo& ti) {
 
 // Tiles of K (rows in kappa order) and V are copied into LDS with buffer loads
 // that write LDS directly; lane i of instruction j of wave w fills the 16-byte
-// chunk (w * DMA_PER_WAVE + j) * 64 + i of the tile.
-struct Rows {
-  __amdgpu_buffer_rsrc_t cache;   // the unit's cache rows [0, len0)
-  __amdgpu_buffer_rsrc_t input;   // the block's rows this workgroup reads
+// chunk (w * DMA_PER_WAVE + j) * 64 + i of the tile.  The buffer resource of a
+// tile's source (cache rows [0, len0) or the block rows the workgroup reads) is
+// built per tile from values forced into scalar registers, so the loads take
+// it straight from SGPRs.
+struct TileSrc {
+  __amdgpu_buffer_rsrc_t rsrc;
 };
 
 // An out-of-range offset: the lane writes zeros (used for the padding slots).
@@ -194,7 +197,7 @@ constexpr int kOutOfRange = 0x7FFFFFF0;
 // holds chunk g % CP of row g / CP; chunks >= CPR are padding.  K rows are
 // stored in kappa order within each 32-row sub-tile.
 template <bool BF16, int D, bool K>
-__device__ __forceinline__ void dma_rows(char* dst, const Rows& rows, const TileInfo& ti,
+__device__ __forceinline__ void dma_rows(char* dst, const TileSrc& src, const TileInfo& ti,
                                          const Geo& s) {
   using C = Cfg<BF16, D>;
   constexpr int CP = K ? C::KCP : C::VCP;   // also the number of 1 KB segments
@@ -206,10 +209,7 @@ __device__ __forceinline__ void dma_rows(char* dst, const Rows& rows, const Tile
       const int r = g / CP, c = g - r * CP;
       const int key = K ? (r & ~31) + kappa(r & 31) : r;
       const int off = c < C::CPR ? (ti.base + key) * C::RB + c * 16 : kOutOfRange;
-      if (ti.cache)   // uniform: one source per tile
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rows.cache, (lds_void*)(dst + seg * 1024), 16, off, 0, 0, 0);
-      else
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rows.input, (lds_void*)(dst + seg * 1024), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src.rsrc, (lds_void*)(dst + seg * 1024), 16, off, 0, 0, 0);
     }
   }
 }
@@ -251,16 +251,26 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       a.pos[(int64_t)s.u * a.cap + a.len0 + r] = a.t0 + r;
   }
 
-  // ---- row sources as buffer resources (out-of-range rows read as zero) ----
-  Rows krows, vrows;
-  krows.cache = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<E*>(static_cast<const E*>(a.kc)) + (int64_t)s.u * a.cap * D, 0, a.len0 * RB, kRsrcWord3);
-  krows.input = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<E*>(static_cast<const E*>(a.kin)) + plane * D, 0, s.in_rows * RB, kRsrcWord3);
-  vrows.cache = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<E*>(static_cast<const E*>(a.vc)) + (int64_t)s.u * a.cap * D, 0, a.len0 * RB, kRsrcWord3);
-  vrows.input = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<E*>(static_cast<const E*>(a.vin)) + plane * D, 0, s.in_rows * RB, kRsrcWord3);
+  // ---- row sources of the tiles (out-of-range rows read as zero) ----
+  const uint64_t kc_base = (uint64_t)(static_cast<const E*>(a.kc) + (int64_t)s.u * a.cap * D);
+  const uint64_t vc_base = (uint64_t)(static_cast<const E*>(a.vc) + (int64_t)s.u * a.cap * D);
+  const uint64_t ki_base = (uint64_t)(static_cast<const E*>(a.kin) + plane * D);
+  const uint64_t vi_base = (uint64_t)(static_cast<const E*>(a.vin) + plane * D);
+  auto tile_src = [&](const TileInfo& ti, bool kside) __device__ {
+    const uint64_t p = ti.cache ? (kside ? kc_base : vc_base) : (kside ? ki_base : vi_base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+    const int nrec = __builtin_amdgcn_readfirstlane((ti.cache ? a.len0 : s.in_rows) * RB);
+    TileSrc r;
+    r.rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nrec, kRsrcWord3);
+    return r;
+  };
+  auto dma_k = [&](char* dst, const TileInfo& ti) __device__ {
+    dma_rows<BF16, D, true>(dst, tile_src(ti, true), ti, s);
+  };
+  auto dma_v = [&](char* dst, const TileInfo& ti) __device__ {
+    dma_rows<BF16, D, false>(dst, tile_src(ti, false), ti, s);
+  };
 
   // ---- query fragments: lane (n, h) holds row n, d-range [h*D/2, (h+1)*D/2) ----
   typename C::qfrag_t qf[C::QSTEPS];
@@ -284,25 +294,29 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   // the row this lane's causal mask uses (padding rows reuse the last real row)
   const int qrow = s.qvalid ? s.row : a.n_tok - 1;
 
-  // logits of one tile: S^T (one query per lane) or S (one key per lane)
-  auto qk_st = [&](const char* ks, f32x16* acc) __device__ {
+  // logits of one tile: S^T (one query per lane) or S (one key per lane); the
+  // K fragments of step kk + 1 are read while the MFMAs of step kk run
+  auto qk_tile = [&](auto st_tag, const char* ks, f32x16* acc) __device__ {
+    constexpr bool ST = decltype(st_tag)::value;
     acc[0] = f32x16{};
     acc[1] = f32x16{};
+    typename C::qfrag_t kf[2][2];
+    kf[0][0] = k_frag<BF16, D>(ks, s.n, s.h, 0);
+    kf[0][1] = k_frag<BF16, D>(ks, 32 + s.n, s.h, 0);
 #pragma unroll
     for (int kk = 0; kk < C::QSTEPS; ++kk) {
-      acc[0] = mfma_step<BF16, D>(k_frag<BF16, D>(ks, s.n, s.h, kk), qf[kk], acc[0]);
-      acc[1] = mfma_step<BF16, D>(k_frag<BF16, D>(ks, 32 + s.n, s.h, kk), qf[kk], acc[1]);
-    }
-  };
-  auto qk_s = [&](const char* ks, f32x16* acc) __device__ {
-    acc[0] = f32x16{};
-    acc[1] = f32x16{};
+      if (kk + 1 < C::QSTEPS) {
+        kf[(kk + 1) & 1][0] = k_frag<BF16, D>(ks, s.n, s.h, kk + 1);
+        kf[(kk + 1) & 1][1] = k_frag<BF16, D>(ks, 32 + s.n, s.h, kk + 1);
+      }
 #pragma unroll
-    for (int kk = 0; kk < C::QSTEPS; ++kk) {
-      acc[0] = mfma_step<BF16, D>(qf[kk], k_frag<BF16, D>(ks, s.n, s.h, kk), acc[0]);
-      acc[1] = mfma_step<BF16, D>(qf[kk], k_frag<BF16, D>(ks, 32 + s.n, s.h, kk), acc[1]);
+      for (int st = 0; st < 2; ++st)
+        acc[st] = ST ? mfma_step<BF16, D>(kf[kk & 1][st], qf[kk], acc[st])
+                     : mfma_step<BF16, D>(qf[kk], kf[kk & 1][st], acc[st]);
     }
   };
+  auto qk_st = [&](const char* ks, f32x16* acc) __device__ { qk_tile(std::true_type{}, ks, acc); };
+  auto qk_s = [&](const char* ks, f32x16* acc) __device__ { qk_tile(std::false_type{}, ks, acc); };
 
   // ======================= sweep 1: online softmax + PV =======================
   f32x16 oacc[C::MT];
@@ -329,25 +343,29 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[st][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float m_new = fmaxf(m_run, tmax * c2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    float psum = 0.0f;
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][r], c2, -m_new));
-        sacc[st][r] = p;
-        psum += p;
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    if (__ballot(alpha != 1.0f) != 0) {
+    // The reference m_run moves only when some row of the wave sees a logit
+    // more than kRescaleLog2 above it: the probabilities stay below
+    // 2^kRescaleLog2 (exact in fp32, fine in bf16) and the O rescale is rare.
+    if (__ballot(tmax * c2 > m_run + kRescaleLog2) != 0) {
+      const float m_new = fmaxf(m_run, tmax * c2);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+      m_run = m_new;
 #pragma unroll
       for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[mt][r] *= alpha;
     }
+    float psum = 0.0f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][r], c2, -m_run));
+        sacc[st][r] = p;
+        psum += p;
+      }
+    l_run += psum;
     if constexpr (BF16) {
       // A operand (V^T): lane (n, h) needs V[key][32 mt + n] for the 8 keys
       // 16 ks + 8 h + e of P's k-slots.  The LDS transpose load gives lane i of
@@ -357,8 +375,23 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       const int j16 = s.lane & 15, dhalf = (s.lane >> 4) & 1;
       const int vrow = 8 * s.h + (j16 >> 2);
       const int vb = (16 * dhalf + 4 * (j16 & 3)) * 2;
+      // the 2 x MT transposing reads of K-step ks4 + 1 are issued before the
+      // MFMAs of step ks4
+      u32x4 vf[2][C::MT];
+      auto vload = [&](int ks4, u32x4* dst) __device__ {
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
+          const int r0 = 16 * ks4 + vrow, b = vb + 64 * mt;
+          const bf16v4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4*)(vs + r0 * C::VSTRIDE + b));
+          const bf16v4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4*)(vs + (r0 + 4) * C::VSTRIDE + b));
+          const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+          dst[mt] = u32x4{l2.x, l2.y, h2.x, h2.y};
+        }
+      };
+      vload(0, vf[0]);
 #pragma unroll
       for (int ks4 = 0; ks4 < 4; ++ks4) {
+        if (ks4 + 1 < 4) vload(ks4 + 1, vf[(ks4 + 1) & 1]);
         const int st = ks4 >> 1, half = ks4 & 1;
         u32x4 pw;
         pw.x = pack_bf16x2(sacc[st][8 * half + 0], sacc[st][8 * half + 1]);
@@ -367,15 +400,9 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         pw.w = pack_bf16x2(sacc[st][8 * half + 6], sacc[st][8 * half + 7]);
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) {
-          const int r0 = 16 * ks4 + vrow, b = vb + 64 * mt;
-          const bf16v4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4*)(vs + r0 * C::VSTRIDE + b));
-          const bf16v4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4*)(vs + (r0 + 4) * C::VSTRIDE + b));
-          const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-          const u32x4 vw = {l2.x, l2.y, h2.x, h2.y};
-          oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb,
+        for (int mt = 0; mt < C::MT; ++mt)
+          oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[ks4 & 1][mt]), pb,
                                                               oacc[mt], 0, 0, 0);
-        }
       }
     } else {
 #pragma unroll
@@ -393,9 +420,9 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   };
 
   // prologue: K(0), V(0), K(1) land in LDS; logits of tile 0
-  dma_rows<BF16, D, true>(kb0, krows, tile_info(a, s, 0), s);
-  dma_rows<BF16, D, false>(vb0, vrows, tile_info(a, s, 0), s);
-  if (nt > 1) dma_rows<BF16, D, true>(kb1, krows, tile_info(a, s, 1), s);
+  dma_k(kb0, tile_info(a, s, 0));
+  dma_v(vb0, tile_info(a, s, 0));
+  if (nt > 1) dma_k(kb1, tile_info(a, s, 1));
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   // logits ping-pong between two register sets; the loop is unrolled by two so
@@ -412,10 +439,10 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     char* v_cur = P == 0 ? vb0 : vb1;
     char* v_fill = P == 0 ? vb1 : vb0;
     const TileInfo ti = tile_info(a, s, t);
-    if (t + 2 < nt) dma_rows<BF16, D, true>(k_fill, krows, tile_info(a, s, t + 2), s);
+    if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2));
     if (t + 1 < nt) {
       const TileInfo tn = tile_info(a, s, t + 1);
-      dma_rows<BF16, D, false>(v_fill, vrows, tn, s);
+      dma_v(v_fill, tn);
       if (tile_active(s, tn)) qk_st(k_next, nxt);
     }
     if (tile_active(s, ti)) {
@@ -488,8 +515,8 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   };
 
   // prologue: K(0), K(1) land in LDS; logits of tile 0
-  dma_rows<BF16, D, true>(kb0, krows, tile_info(a, s, 0), s);
-  if (nt > 1) dma_rows<BF16, D, true>(kb1, krows, tile_info(a, s, 1), s);
+  dma_k(kb0, tile_info(a, s, 0));
+  if (nt > 1) dma_k(kb1, tile_info(a, s, 1));
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   if (tile_active(s, tile_info(a, s, 0))) qk_s(kb0, sa);
@@ -501,7 +528,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     char* k_next = P == 0 ? kb1 : kb0;
     float (*cs)[kKeyTile] = P == 0 ? cs0 : cs1;
     const TileInfo ti = tile_info(a, s, t);
-    if (t + 2 < nt) dma_rows<BF16, D, true>(k_fill, krows, tile_info(a, s, t + 2), s);
+    if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2));
     if (t + 1 < nt) {
       const TileInfo tn = tile_info(a, s, t + 1);
       if (tile_active(s, tn)) qk_s(k_next, nxt);

@@ -32,6 +32,54 @@ if ROOT not in sys.path:
 PEAK_BF16_MFMA = 2.5e15      # dense bf16 MFMA, FLOP/s
 PEAK_F32_MFMA = 157.3e12     # fp32 matrix/vector, FLOP/s
 PEAK_HBM = 8.0e12            # bytes/s
+HBM_PROBE_BYTES = 1 << 30    # the plain copy that calibrates the HBM byte counters
+
+
+def source_digest() -> str:
+    """sha256 over the prefill kernel's sources: a counter record applies only
+    to the kernel it was measured on."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for rel in ("paper_2412_05693_amd/csrc/k_prefill.hip", "paper_2412_05693_amd/csrc/bm_internal.h"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per prefill launch from a committed counter record
+    (`traffic-record:` line under profiles/), or None when there is none for
+    this workload or the kernel sources changed since it was taken."""
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None
+    digest = source_digest()
+    for fn in sorted(os.listdir(pdir)):
+        if not fn.endswith((".md", ".txt")):
+            continue
+        with open(os.path.join(pdir, fn)) as f:
+            for line in f:
+                line = line.strip().strip("`")
+                if not line.startswith("traffic-record:"):
+                    continue
+                kv = dict(item.split("=", 1) for item in line.split()[1:] if "=" in item)
+                if kv.get("workload") == workload and kv.get("source_sha256") == digest:
+                    return int(kv["bytes_per_launch"])
+    return None
+
+
+def hbm_probe():
+    """A plain device copy of HBM_PROBE_BYTES, three times: run it under
+    rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) to calibrate the counters."""
+    import torch
+
+    a = torch.ones(HBM_PROBE_BYTES, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(f"hbm probe: copied {HBM_PROBE_BYTES} bytes three times", flush=True)
 
 
 # ---------------------------------------------------------------------------
@@ -164,8 +212,9 @@ def gpu_bench(name, overrides, steps, warmup):
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd = kernels[dom]
+    traffic = measured_traffic(wl.name) if dom == "prefill_attention" else None
     roofline = {"bound": kd["bound"], "achieved": round(kd["achieved"], 3), "peak": kd["peak"],
-                "unit": kd["unit"], "frac": round(kd["frac"], 5), "traffic": None,
+                "unit": kd["unit"], "frac": round(kd["frac"], 5), "traffic": traffic,
                 "kernel": dom}
     tokens = wl.b * (wl.s + wl.n_decode)
     return {
@@ -188,7 +237,12 @@ def main():
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hbm-probe", action="store_true",
+                    help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
+    if args.hbm_probe:
+        hbm_probe()
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
               "the path shards with no communication and is not run across GPUs here.",

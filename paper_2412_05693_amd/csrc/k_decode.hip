@@ -139,7 +139,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 
   // first batch of V rows for phase 4, in flight during the softmax
   constexpr int NKL4 = 256 / CPR;
-  constexpr int UNR = 4;
+  constexpr int UNR = 8;   // V rows per thread in flight (and as many prefetched)
   const int c4 = tid % CPR, kl4 = tid / CPR;
   u32x4 vw[UNR];
 #pragma unroll

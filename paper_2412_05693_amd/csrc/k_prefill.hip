@@ -559,18 +559,22 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 
 // Fold the per-workgroup partial column sums into the scores, in workgroup
 // order: score[j] = (j < len0 ? score[j] : 0) + sum over workgroups that saw j.
+// Grid: (units, slot chunks of 256); every thread owns one slot and issues its
+// partial-sum loads together.
 __global__ void __launch_bounds__(256) score_reduce_kernel(PrefillArgs a, int pt_positions) {
   const int u = blockIdx.x;
   const int n = a.len0 + a.n_tok;
-  const float* part = a.partial + (int64_t)u * a.npt_stride * a.cap;
-  float* score = a.score + (int64_t)u * a.cap;
-  for (int j = threadIdx.x; j < n; j += blockDim.x) {
+  const int j = blockIdx.y * 256 + threadIdx.x;
+  if (j < n) {
+    const float* part = a.partial + (int64_t)u * a.npt_stride * a.cap + j;
+    float* score = a.score + (int64_t)u * a.cap;
     const int pt0 = j < a.len0 ? 0 : (j - a.len0) / pt_positions;
     float acc = j < a.len0 ? score[j] : 0.0f;
-    for (int pt = pt0; pt < a.npt_used; ++pt) acc += part[(int64_t)pt * a.cap + j];
+#pragma unroll 8
+    for (int pt = pt0; pt < a.npt_used; ++pt) acc += part[(int64_t)pt * a.cap];
     score[j] = acc;
   }
-  if (threadIdx.x == 0) a.len[u] = n;
+  if (blockIdx.y == 0 && threadIdx.x == 0) a.len[u] = n;
 }
 
 template <bool BF16, int D, int G>
@@ -606,8 +610,9 @@ hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int gro
 
 hipError_t launch_score_reduce(const PrefillArgs& a, hipStream_t stream) {
   const int group = a.n_heads / a.n_kv_heads;
-  hipLaunchKernelGGL(score_reduce_kernel, dim3((unsigned)a.units), dim3(256), 0, stream, a,
-                     positions_per_wg(group));
+  const unsigned chunks = (unsigned)((a.len0 + a.n_tok + 255) / 256);
+  hipLaunchKernelGGL(score_reduce_kernel, dim3((unsigned)a.units, chunks), dim3(256), 0, stream,
+                     a, positions_per_wg(group));
   return hipGetLastError();
 }
 

@@ -13,7 +13,14 @@ launch time measured with HIP events on the launch stream), and the CPU
 baseline (the float64 oracle on a bounded sample of units, timed on the host
 before the GPU is initialised).
 
-    python bench.py [--config c2] [--steps K] [--warmup W] [--gpus 1]
+    python bench.py [--config c5] [--steps K] [--warmup W] [--gpus 1] [--batch B]
+
+Default workload: c5, the 32-layer Llama-3-8B-shaped attention stack (GQA
+32/8, d 128, s 8192, bound 512, block 256, 256 decode steps) at the largest
+batch whose bounded caches and block buffers fit the device's free memory; its
+prompt inputs are evaluated per (layer, block) on the device by the
+counter-based generator (bm_synth.h), whose time is measured and excluded from
+the throughput.  c1-c4 are the single-layer workloads with resident inputs.
 """
 from __future__ import annotations
 
@@ -86,17 +93,22 @@ def hbm_probe():
 # CPU baseline: the oracle as it stands, one unit per worker process
 # ---------------------------------------------------------------------------
 def _oracle_unit(args):
-    name, overrides, bi, hk = args
-    os.environ.setdefault("OMP_NUM_THREADS", "1")
+    name, overrides, layer, bi, hk = args
+    from threadpoolctl import threadpool_limits
+
     from oracle import pd as opd
     from paper_2412_05693_amd import synth
 
     wl = synth.WORKLOADS[name].with_(**overrides)
-    q, k, v = synth.unit_inputs(wl, 0, bi, hk)
-    t = time.perf_counter()
-    opd.run_unit(q, k, v, s=wl.s, kv_max=wl.kv_max, block=wl.block, n_decode=wl.n_decode,
-                 sm_scale=wl.sm_scale)
-    return time.perf_counter() - t
+    if wl.n_layers > 1:
+        q, k, v = synth.stack_unit_inputs(wl, layer, bi, hk)
+    else:
+        q, k, v = synth.unit_inputs(wl, layer, bi, hk)
+    with threadpool_limits(1):     # one unit per process, one BLAS thread each
+        t = time.perf_counter()
+        opd.run_unit(q, k, v, s=wl.s, kv_max=wl.kv_max, block=wl.block, n_decode=wl.n_decode,
+                     sm_scale=wl.sm_scale)
+        return time.perf_counter() - t
 
 
 def cpu_baseline(name, overrides, budget_s):
@@ -109,24 +121,35 @@ def cpu_baseline(name, overrides, budget_s):
         os.environ[var] = "1"
     ctx = mp.get_context("fork")     # forked before any GPU initialisation
     units = synth.checked_units(wl, min(wl.units, 100000), seed=7)
+    if wl.n_layers > 1:               # spread the sample over the layers too
+        units = [((i * 7919) % wl.n_layers, bi, hk) for i, (bi, hk) in enumerate(units)]
+    else:
+        units = [(0, bi, hk) for (bi, hk) in units]
+    total_units = wl.units * wl.n_layers
     done, t0 = 0, time.perf_counter()
+    unit_s = 0.0
     with ctx.Pool(cores) as pool:
         # first wave sizes the sample: keep to about budget_s of wall time
-        first = pool.map(_oracle_unit, [(name, overrides, bi, hk) for (bi, hk) in units[:cores]])
+        first = pool.map(_oracle_unit, [(name, overrides) + u for u in units[:cores]])
         per_unit = sum(first) / len(first)
         want = max(cores, int(budget_s * cores / max(per_unit, 1e-6)))
         want = min(want, len(units))
         rest = units[cores:want]
-        if rest:
-            pool.map(_oracle_unit, [(name, overrides, bi, hk) for (bi, hk) in rest])
+        more = pool.map(_oracle_unit, [(name, overrides) + u for u in rest]) if rest else []
         done = cores + len(rest)
+        unit_s = sum(first) + sum(more)
     wall = time.perf_counter() - t0
-    t_full = wall * wl.units / done          # units are independent and equal in cost
+    # units are independent and equal in cost: the oracle time of the whole
+    # workload is the sampled units' oracle time scaled to all units, spread
+    # over the same number of processes
+    t_full = unit_s / done * total_units / cores
     tok = wl.b * (wl.s + wl.n_decode)
+    what = "(layer, sample, KV head)" if wl.n_layers > 1 else "(sample, KV head)"
     return {"value": tok / t_full, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} of {wl.units} (sample, KV head) units of {wl.name}, full P&D "
-                      f"each, float64 numpy, one unit per process; {wall:.1f} s wall, "
-                      f"scaled to all units"}
+            "sample": f"{done} of {total_units} {what} units of {wl.name} (b={wl.b}), full P&D "
+                      f"each, float64 numpy, one unit per process and one BLAS thread; "
+                      f"{unit_s:.1f} s of oracle time in {wall:.1f} s wall, scaled to all "
+                      f"units over {cores} processes"}
 
 
 # ---------------------------------------------------------------------------
@@ -229,17 +252,172 @@ def gpu_bench(name, overrides, steps, warmup):
     }
 
 
+STACK_RESERVE = 3 << 30      # device bytes left to the runtime when planning the batch
+
+
+def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
+    """The layer stack at the largest batch that fits: per (layer, block) the
+    device generator writes the block's Q/K/V, then prefill and the cut; then
+    the decode steps, layer by layer.  Generator time is measured and left out
+    of the throughput (the inputs of a resident workload are not generated)."""
+    import torch
+
+    from paper_2412_05693_amd import batchmax as bmx
+    from paper_2412_05693_amd import synth
+
+    wl = synth.WORKLOADS[name].with_(**overrides)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    shape = dict(n_layers=wl.n_layers, s=wl.s, kv_max=wl.kv_max, block=wl.block,
+                 max_gen=wl.n_decode, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads,
+                 head_dim=wl.head_dim, dtype=wl.dtype)
+    free, total = torch.cuda.mem_get_info(dev)
+    budget = free - STACK_RESERVE
+    b_plan = bmx.plan_stack_batch(budget, **shape)
+    es = 4 if wl.dtype == "f32" else 2
+    io_per_sample = (wl.block + 1) * (2 * wl.n_heads + 2 * wl.n_kv_heads) * wl.head_dim * es
+    b_do = int(budget // (bmx.full_cache_bytes_per_sample(
+        n_layers=wl.n_layers, s=wl.s, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+        dtype=wl.dtype) + io_per_sample))
+    b = batch if batch else b_plan
+    wl = wl.with_(b=b)
+    print(f"[bench] {wl.name}: device free {free / 1e9:.1f} GB of {total / 1e9:.1f} GB; "
+          f"max batch {b_plan} (decoding-only compression: {b_do}); running b={b}", flush=True)
+    stack = bmx.PDStack(n_layers=wl.n_layers, b=b, s=wl.s, kv_max=wl.kv_max, block=wl.block,
+                        max_gen=wl.n_decode, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads,
+                        head_dim=wl.head_dim, dtype=wl.dtype, sm_scale=wl.sm_scale, device=dev)
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    H, Hk, d, B = wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.block
+    q = torch.empty((b, H, B, d), dtype=tdt, device=dev)
+    k = torch.empty((b, Hk, B, d), dtype=tdt, device=dev)
+    v = torch.empty_like(k)
+    o = torch.empty_like(q)
+    qd = torch.empty((b, H, 1, d), dtype=tdt, device=dev)
+    kd = torch.empty((b, Hk, 1, d), dtype=tdt, device=dev)
+    vd = torch.empty_like(kd)
+    od = torch.empty_like(qd)
+    params = [bmx.synth_params(b=b, n_heads=H, n_kv_heads=Hk, head_dim=d, dtype=wl.dtype,
+                               seed=wl.seed, layer=layer, s=wl.s, hh_frac=wl.hh_frac,
+                               hh_scale=wl.hh_scale, n_sinks=wl.n_sinks,
+                               sink_scale=wl.sink_scale, heavy=wl.hh_mode != "none")
+              for layer in range(wl.n_layers)]
+    stream = torch.cuda.current_stream(dev)
+    blocks = [(t0, min(B, wl.s - t0)) for t0 in range(0, wl.s, B)]
+    L = wl.n_layers
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+
+    def one_step(timed):
+        ev = {"gen": [], "pf": [], "cut": [], "dec": []} if timed else None
+
+        def rec(kind, fn):
+            if ev is None:
+                fn()
+                return
+            a, z = mk(), mk()
+            a.record(stream)
+            fn()
+            z.record(stream)
+            ev[kind].append((a, z))
+
+        stack.reset()
+        for (t0, n) in blocks:
+            for layer in range(L):
+                pd = stack.layers[layer]
+                rec("gen", lambda: bmx.synth_qkv(params[layer], t0, q, k, v))
+                rec("pf", lambda: pd.prefill_block(t0, n, q, k, v, o, row=0))
+                rec("cut", lambda: pd.evict_compact(t0 + n - 1))
+        for t in range(wl.n_decode):
+            p = wl.s + t
+            for layer in range(L):
+                pd = stack.layers[layer]
+                rec("gen", lambda: bmx.synth_qkv(params[layer], p, qd, kd, vd))
+                rec("dec", lambda: pd.decode_step(p, qd, kd, vd, od, row=0))
+        return ev
+
+    for _ in range(warmup):
+        one_step(False)
+    torch.cuda.synchronize()
+    evs, walls = [], []
+    for _ in range(steps):
+        torch.cuda.synchronize()
+        t0w = time.perf_counter()
+        evs.append(one_step(True))
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0w)
+
+    def ms(kind):
+        return sum(a.elapsed_time(z) for e in evs for (a, z) in e[kind]) / steps
+
+    gen_ms, pf_ms, ev_ms, dec_ms = ms("gen"), ms("pf"), ms("cut"), ms("dec")
+    wall_ms = sum(walls) * 1e3 / steps
+    ms_step = wall_ms - gen_ms
+    G = wl.group
+    flops = L * bmx.prefill_flops(b=b, n_kv_heads=Hk, group=G, head_dim=d, s=wl.s,
+                                  kv_max=wl.kv_max, block=B)
+    dbytes = L * bmx.decode_bytes_per_step(b=b, n_kv_heads=Hk, group=G, head_dim=d,
+                                           kv_max=wl.kv_max, elem_bytes=es)
+    peak_f = PEAK_F32_MFMA if wl.dtype == "f32" else PEAK_BF16_MFMA
+    prefill_tflops = flops / (pf_ms * 1e-3) / 1e12
+    decode_gbs = dbytes * wl.n_decode / (dec_ms * 1e-3) / 1e9
+    n_pf = L * len(blocks)
+    kernels = {
+        "prefill_attention": {"bound": "mfma", "achieved": prefill_tflops,
+                              "peak": peak_f / 1e12, "unit": "TFLOP/s",
+                              "frac": prefill_tflops / (peak_f / 1e12),
+                              "ms_per_step": pf_ms, "launches_per_step": n_pf,
+                              "algorithmic_per_launch": flops / n_pf},
+        "evict_compact": {"ms_per_step": ev_ms, "launches_per_step": n_pf},
+        "decode_step": {"bound": "hbm", "achieved": decode_gbs, "peak": PEAK_HBM / 1e9,
+                        "unit": "GB/s", "frac": decode_gbs / (PEAK_HBM / 1e9),
+                        "ms_per_step": dec_ms, "launches_per_step": L * wl.n_decode,
+                        "algorithmic_per_launch": dbytes / L},
+    }
+    dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
+    kd_ = kernels[dom]
+    traffic = measured_traffic(wl.name) if dom == "prefill_attention" else None
+    roofline = {"bound": kd_["bound"], "achieved": round(kd_["achieved"], 3), "peak": kd_["peak"],
+                "unit": kd_["unit"], "frac": round(kd_["frac"], 5), "traffic": traffic,
+                "kernel": dom}
+    tokens = b * (wl.s + wl.n_decode)
+    stack.close()
+    return {
+        "value": tokens / (ms_step * 1e-3),
+        "ms_per_step": ms_step,
+        "roofline": roofline,
+        "kernels": kernels,
+        "phases": {"prefill_tokens_per_s": b * wl.s / ((pf_ms + ev_ms) * 1e-3),
+                   "decode_tokens_per_s": b * wl.n_decode / (dec_ms * 1e-3),
+                   "generated_tokens_per_s": b * wl.n_decode / (ms_step * 1e-3),
+                   "input_generation_ms_per_step": gen_ms,
+                   "wall_ms_per_step_with_generation": wall_ms},
+        "stack": {"n_layers": L, "max_batch": b_plan, "max_batch_decoding_only": b_do,
+                  "device_free_bytes": free, "arena_bytes": stack.arena_bytes},
+        "workload": wl,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4"])
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 10; 1 for the layer stack)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps first (default 2; 1 for the layer stack)")
+    ap.add_argument("--config", default="c5", choices=["c1", "c2", "c3", "c4", "c5"],
+                    help="workload (default c5: the 32-layer stack at the largest batch that "
+                         "fits, the configuration the metric is quoted at)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="layer stack only: run this batch instead of the largest that fits")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
+    stack = args.config == "c5"
+    if args.steps is None:
+        args.steps = 1 if stack else 10
+    if args.warmup is None:
+        args.warmup = 1 if stack else 2
     if args.hbm_probe:
         hbm_probe()
         return
@@ -253,10 +431,14 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, overrides, args.cpu_seconds)
-    res = gpu_bench(args.config, overrides, args.steps, args.warmup)
+    if args.config == "c5":
+        res = gpu_bench_stack(args.config, overrides, args.steps, args.warmup, args.batch)
+    else:
+        res = gpu_bench(args.config, overrides, args.steps, args.warmup)
     wl = res["workload"]
     line = {
-        "metric": "P&D tokens/s (prefill+decode)",
+        "metric": ("P&D tokens/s (prefill+decode) at max batch; prefill MFMA %, decode HBM GB/s"
+                   if "stack" in res else "P&D tokens/s (prefill+decode)"),
         "value": round(res["value"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -277,6 +459,10 @@ def main():
         "kernels": res["kernels"],
         "phases": res["phases"],
     }
+    if "stack" in res:
+        line["config"]["n_layers"] = res["stack"]["n_layers"]
+        line["config"]["max_batch_decoding_only"] = res["stack"]["max_batch_decoding_only"]
+        line["stack"] = res["stack"]
     print(json.dumps(line), flush=True)
 
 

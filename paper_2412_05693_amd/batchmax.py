@@ -41,6 +41,14 @@ class bm_dims(ctypes.Structure):
                 ("sm_scale", ctypes.c_float)]
 
 
+class bm_synth(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("seed", ctypes.c_uint32),
+                ("layer", ctypes.c_int32), ("s", ctypes.c_int32), ("hh_threshold", ctypes.c_uint32),
+                ("hh_scale", ctypes.c_float), ("n_sinks", ctypes.c_int32),
+                ("sink_scale", ctypes.c_float), ("value_scale", ctypes.c_float)]
+
+
 class bm_cache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("score", ctypes.c_void_p),
                 ("pos", ctypes.c_void_p), ("len", ctypes.c_void_p), ("work", ctypes.c_void_p),
@@ -73,6 +81,8 @@ def _load() -> ctypes.CDLL:
         "bm_ctx_len": (I32, [P]),
         "bm_ctx_next_pos": (I32, [P]),
         "bm_destroy": (None, [P]),
+        "bm_synth_qkv": (ctypes.c_int, [ctypes.POINTER(bm_synth), I32, I32, P, P, P, I32, P]),
+        "bm_philox4x32_10": (ctypes.c_int, [P, P, ctypes.c_int64, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -84,7 +94,8 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
             "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block", "bm_evict_compact",
-            "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy")
+            "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
+            "bm_philox4x32_10")
 
 
 def _check(status: int) -> None:
@@ -154,6 +165,15 @@ def bm_destroy(ctx: int) -> None:
     _lib.bm_destroy(ctx)
 
 
+def bm_synth_qkv(params: bm_synth, t0: int, n_rows: int, q: int, k: int, v: int, seq_ld: int,
+                 stream: int) -> None:
+    _check(_lib.bm_synth_qkv(ctypes.byref(params), t0, n_rows, q, k, v, seq_ld, stream))
+
+
+def bm_philox4x32_10(inp: int, out: int, n: int, stream: int) -> None:
+    _check(_lib.bm_philox4x32_10(inp, out, n, stream))
+
+
 def make_dims(*, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim, dtype,
               sm_scale=0.0) -> bm_dims:
     dt = {"f32": BM_F32, "bf16": BM_BF16}.get(dtype, dtype)
@@ -173,7 +193,7 @@ class PDAttention:
     """
 
     def __init__(self, *, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim,
-                 dtype="bf16", sm_scale=0.0, device="cuda", init=True):
+                 dtype="bf16", sm_scale=0.0, device="cuda", init=True, buffers=None):
         import torch
 
         self.torch = torch
@@ -189,13 +209,26 @@ class PDAttention:
         self.cap = bm_cache_slots(self.dims)
         self.group = n_heads // n_kv_heads
         U = b * n_kv_heads
-        self.k = torch.empty((b, n_kv_heads, self.cap, head_dim), dtype=self.tdtype, device=self.device)
-        self.v = torch.empty_like(self.k)
-        self.score = torch.empty((b, n_kv_heads, self.cap), dtype=torch.float32, device=self.device)
-        self.pos = torch.zeros((b, n_kv_heads, self.cap), dtype=torch.int32, device=self.device)
-        self.len = torch.empty((b, n_kv_heads), dtype=torch.int32, device=self.device)
         self.work_bytes = bm_workspace_bytes(self.dims)
-        self.work = torch.empty(self.work_bytes, dtype=torch.uint8, device=self.device)
+        if buffers is None:
+            self.k = torch.empty((b, n_kv_heads, self.cap, head_dim), dtype=self.tdtype, device=self.device)
+            self.v = torch.empty_like(self.k)
+            self.score = torch.empty((b, n_kv_heads, self.cap), dtype=torch.float32, device=self.device)
+            self.pos = torch.zeros((b, n_kv_heads, self.cap), dtype=torch.int32, device=self.device)
+            self.len = torch.empty((b, n_kv_heads), dtype=torch.int32, device=self.device)
+            self.work = torch.empty(self.work_bytes, dtype=torch.uint8, device=self.device)
+        else:
+            # caller-provided views (for example slices of one arena); shapes checked
+            self.k, self.v, self.score, self.pos, self.len, self.work = buffers
+            want = {"k": (b, n_kv_heads, self.cap, head_dim), "v": (b, n_kv_heads, self.cap, head_dim),
+                    "score": (b, n_kv_heads, self.cap), "pos": (b, n_kv_heads, self.cap),
+                    "len": (b, n_kv_heads)}
+            for nm, shp in want.items():
+                x = getattr(self, nm)
+                if tuple(x.shape) != shp or not x.is_contiguous() or x.device != self.device:
+                    raise ValueError(f"buffer {nm}: need a contiguous {shp} tensor on {self.device}")
+            if self.work.numel() * self.work.element_size() < self.work_bytes:
+                raise ValueError("work buffer is smaller than bm_workspace_bytes")
         self.cache = bm_cache(self.k.data_ptr(), self.v.data_ptr(), self.score.data_ptr(),
                               self.pos.data_ptr(), self.len.data_ptr(), self.work.data_ptr(),
                               self.work_bytes)
@@ -293,6 +326,145 @@ class PDAttention:
             self.close()
         except Exception:
             pass
+
+
+# ---------------------------------------------------------------------------
+# synthetic inputs of the layer stack (bm_synth.h)
+# ---------------------------------------------------------------------------
+def synth_params(*, b, n_heads, n_kv_heads, head_dim, dtype, seed, layer, s, hh_frac=0.02,
+                 hh_scale=4.0, n_sinks=0, sink_scale=6.0, heavy=True) -> bm_synth:
+    """Generator parameters: value_scale = float32(sqrt(3) / sqrt(d) / 65536) and
+    hh_threshold = round(hh_frac * 2^32) (0 when there are no heavy hitters)."""
+    dt = {"f32": BM_F32, "bf16": BM_BF16}.get(dtype, dtype)
+    thr = int(round(hh_frac * 2.0 ** 32)) if heavy else 0
+    vs = ctypes.c_float(math.sqrt(3.0) / math.sqrt(head_dim) / 65536.0).value
+    return bm_synth(b, n_heads, n_kv_heads, head_dim, dt, seed, layer, s, thr, hh_scale, n_sinks,
+                    sink_scale, vs)
+
+
+def synth_qkv(params: bm_synth, t0: int, q, k, v) -> None:
+    """Fill every row of q [b, H, T, d], k/v [b, Hk, T, d] (torch, contiguous, on one
+    GPU) with the stream's rows for positions t0 .. t0+T-1, on the current stream."""
+    import torch
+
+    tdt = torch.float32 if params.dtype == BM_F32 else torch.bfloat16
+    T = q.shape[2]
+    for x, hh, nm in ((q, params.n_heads, "q"), (k, params.n_kv_heads, "k"), (v, params.n_kv_heads, "v")):
+        if x.dtype != tdt or not x.is_contiguous() or x.device.type != "cuda" or \
+                tuple(x.shape) != (params.b, hh, T, params.head_dim):
+            raise ValueError(f"{nm}: need a contiguous {tdt} [b, {hh}, {T}, d] tensor on the GPU")
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    bm_synth_qkv(params, t0, T, q.data_ptr(), k.data_ptr(), v.data_ptr(), T, stream)
+
+
+# ---------------------------------------------------------------------------
+# a stack of layers: one bounded cache per layer in a single device arena
+# ---------------------------------------------------------------------------
+def _align(n: int, a: int = 256) -> int:
+    return (n + a - 1) // a * a
+
+
+def stack_layer_bytes(*, b, kv_max, block, n_kv_heads, head_dim, dtype) -> int:
+    """Device bytes of one layer's cache (K, V, score, pos, len), 256-byte aligned."""
+    cap = kv_max + block
+    es = 4 if dtype in ("f32", BM_F32) else 2
+    rows = b * n_kv_heads * cap
+    return (2 * _align(rows * head_dim * es) + 2 * _align(rows * 4) + _align(b * n_kv_heads * 4))
+
+
+class PDStack:
+    """``n_layers`` independent bounded caches (the attention layers of one
+    model, each with its own scores and evictions) carved from one device
+    arena, sharing one workspace (its contents never outlive a call).  Layer
+    ``l`` is driven through ``self.layers[l]``, a ``PDAttention``."""
+
+    def __init__(self, *, n_layers, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim,
+                 dtype="bf16", sm_scale=0.0, device="cuda"):
+        import torch
+
+        dims = make_dims(b=b, s=s, kv_max=kv_max, block=block, max_gen=max_gen, n_heads=n_heads,
+                         n_kv_heads=n_kv_heads, head_dim=head_dim, dtype=dtype, sm_scale=sm_scale)
+        bm_validate_dims(dims)
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        tdt = torch.float32 if dims.dtype == BM_F32 else torch.bfloat16
+        es = 4 if dims.dtype == BM_F32 else 2
+        cap = kv_max + block
+        per_layer = stack_layer_bytes(b=b, kv_max=kv_max, block=block, n_kv_heads=n_kv_heads,
+                                      head_dim=head_dim, dtype=dims.dtype)
+        work_bytes = bm_workspace_bytes(dims)
+        self.arena_bytes = n_layers * per_layer + _align(work_bytes)
+        self.arena = torch.empty(self.arena_bytes, dtype=torch.uint8, device=dev)
+        work = self.arena[n_layers * per_layer:n_layers * per_layer + work_bytes]
+        rows = b * n_kv_heads * cap
+        self.layers = []
+        for layer in range(n_layers):
+            off = layer * per_layer
+
+            def take(nbytes, dt, shape):
+                nonlocal off
+                x = self.arena[off:off + nbytes].view(dt).view(shape)
+                off += _align(nbytes)
+                return x
+
+            kk = take(rows * head_dim * es, tdt, (b, n_kv_heads, cap, head_dim))
+            vv = take(rows * head_dim * es, tdt, (b, n_kv_heads, cap, head_dim))
+            sc = take(rows * 4, torch.float32, (b, n_kv_heads, cap))
+            ps = take(rows * 4, torch.int32, (b, n_kv_heads, cap))
+            ln = take(b * n_kv_heads * 4, torch.int32, (b, n_kv_heads))
+            self.layers.append(PDAttention(b=b, s=s, kv_max=kv_max, block=block, max_gen=max_gen,
+                                           n_heads=n_heads, n_kv_heads=n_kv_heads,
+                                           head_dim=head_dim, dtype=dtype, sm_scale=sm_scale,
+                                           device=dev, init=False,
+                                           buffers=(kk, vv, sc, ps, ln, work)))
+        self.n_layers = n_layers
+        self.device = dev
+
+    def reset(self) -> None:
+        for layer in self.layers:
+            layer.reset()
+
+    def close(self) -> None:
+        for layer in self.layers:
+            layer.close()
+
+
+def stack_bytes(*, b, n_layers, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim,
+                dtype) -> int:
+    """Device bytes a P&D run of the layer stack needs at batch b: every layer's
+    bounded cache, the shared workspace, and the reusable input/output buffers
+    of one prefill block and one decode row."""
+    es = 4 if dtype in ("f32", BM_F32) else 2
+    dims = make_dims(b=b, s=s, kv_max=kv_max, block=block, max_gen=max_gen, n_heads=n_heads,
+                     n_kv_heads=n_kv_heads, head_dim=head_dim, dtype=dtype)
+    caches = n_layers * stack_layer_bytes(b=b, kv_max=kv_max, block=block, n_kv_heads=n_kv_heads,
+                                          head_dim=head_dim, dtype=dtype)
+    work = _align(bm_workspace_bytes(dims))
+    rows = block + 1
+    io = rows * b * (2 * n_heads + 2 * n_kv_heads) * head_dim * es
+    return caches + work + io
+
+
+def full_cache_bytes_per_sample(*, n_layers, s, n_kv_heads, head_dim, dtype) -> int:
+    """K and V of every prompt position of every layer: the memory a
+    decoding-only compression scheme holds before its first decode step."""
+    es = 4 if dtype in ("f32", BM_F32) else 2
+    return n_layers * n_kv_heads * s * head_dim * es * 2
+
+
+def plan_stack_batch(budget_bytes: int, **shape) -> int:
+    """Largest b with stack_bytes(b, **shape) <= budget_bytes (0 if none)."""
+    lo, hi = 0, 1
+    while stack_bytes(b=hi, **shape) <= budget_bytes:
+        lo, hi = hi, hi * 2
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        if stack_bytes(b=mid, **shape) <= budget_bytes:
+            lo = mid
+        else:
+            hi = mid
+    return lo
 
 
 # ---------------------------------------------------------------------------

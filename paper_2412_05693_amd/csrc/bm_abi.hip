@@ -342,6 +342,55 @@ BM_EXPORT int32_t bm_ctx_next_pos(const bm_ctx* ctx) { return ctx ? ctx->next_po
 BM_EXPORT void bm_destroy(bm_ctx* ctx) { delete ctx; }
 
 // ---------------------------------------------------------------------------
+// synthetic inputs of the layer stack (bm_synth.h)
+// ---------------------------------------------------------------------------
+BM_EXPORT int bm_synth_qkv(const bm_synth* p, int32_t t0, int32_t n_rows, void* q, void* k,
+                           void* v, int32_t seq_ld, hipStream_t stream) {
+  if (!p) return fail(BM_ERR_INVALID_ARG, "params are null");
+  if (!q || !k || !v) return fail(BM_ERR_INVALID_ARG, "q, k or v is null");
+  if (p->b < 1 || p->n_heads < 1 || p->n_kv_heads < 1 || p->head_dim < 2 || (p->head_dim & 1))
+    return fail(BM_ERR_INVALID_ARG, "b, heads must be positive and head_dim even");
+  if (p->dtype != BM_F32 && p->dtype != BM_BF16)
+    return fail(BM_ERR_INVALID_ARG, "dtype %d is neither BM_F32 nor BM_BF16", p->dtype);
+  if (t0 < 0 || n_rows < 1 || seq_ld < n_rows)
+    return fail(BM_ERR_INVALID_ARG, "t0=%d n_rows=%d seq_ld=%d", t0, n_rows, seq_ld);
+  if ((int64_t)(t0 + n_rows) * (p->head_dim / 2) > 0xFFFFFFFFll)
+    return fail(BM_ERR_INVALID_ARG, "positions beyond the 32-bit counter word");
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v) & 3)
+    return fail(BM_ERR_INVALID_ARG, "q, k and v must be 4-byte aligned");
+  bm::SynthArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.b = p->b;
+  a.n_heads = p->n_heads;
+  a.n_kv_heads = p->n_kv_heads;
+  a.head_dim = p->head_dim;
+  a.dtype = p->dtype;
+  a.layer = p->layer;
+  a.s = p->s;
+  a.n_sinks = p->n_sinks;
+  a.t0 = t0;
+  a.n_rows = n_rows;
+  a.seq_ld = seq_ld;
+  a.seed = p->seed;
+  a.hh_threshold = p->hh_threshold;
+  a.hh_scale = p->hh_scale;
+  a.sink_scale = p->sink_scale;
+  a.value_scale = p->value_scale;
+  const hipError_t e = bm::launch_synth_qkv(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "synth launch");
+  return ok();
+}
+
+BM_EXPORT int bm_philox4x32_10(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t stream) {
+  if (!in || !out || n < 1) return fail(BM_ERR_INVALID_ARG, "in, out null or n < 1");
+  const hipError_t e = bm::launch_philox(in, out, n, stream);
+  if (e != hipSuccess) return hip_fail(e, "philox launch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 // cache reset: a fill kernel rather than hipMemsetAsync, so the enqueued work
 // is safe to record into a HIP graph
 // ---------------------------------------------------------------------------

@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "batchmax.h"
+#include "bm_synth.h"
 
 namespace bm {
 
@@ -78,6 +79,16 @@ struct DecodeArgs {
   float scale_log2;
 };
 
+struct SynthArgs {
+  void* q;
+  void* k;
+  void* v;
+  int b, n_heads, n_kv_heads, head_dim, dtype, layer, s, n_sinks, t0, n_rows;
+  int64_t seq_ld;
+  uint32_t seed, hh_threshold;
+  float hh_scale, sink_scale, value_scale;
+};
+
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int group,
                           hipStream_t stream);
 hipError_t launch_score_reduce(const PrefillArgs& a, hipStream_t stream);
@@ -87,5 +98,7 @@ hipError_t launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group
                          hipStream_t stream);
 hipError_t launch_reset(float* score, int32_t* len, size_t n_score, size_t n_len,
                         hipStream_t stream);
+hipError_t launch_synth_qkv(const SynthArgs& a, hipStream_t stream);
+hipError_t launch_philox(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t stream);
 
 }  // namespace bm

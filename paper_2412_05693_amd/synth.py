@@ -22,6 +22,20 @@ positions come from ``SeedSequence([seed, 1, layer, sample])``.  Bulk units of
 large configurations are drawn on the device with ``torch.randn`` (timing
 only, same distributions and the same heavy-hitter positions); checked units
 are overwritten with the host stream so the oracle can reproduce them.
+
+The 32-layer stack (c5) cannot hold its prompt inputs (3.2 GB per sample), so
+its Q/K/V come from a counter-based stream that the device evaluates per block
+and this module evaluates for checked units: Philox4x32-10 (Salmon, Moraes,
+Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011).  Each
+call yields two elements; an element is the Irwin-Hall sum S of four 16-bit
+uniforms, z = (S - 131070) * c with c = float32(sqrt(3) / sqrt(d) / 65536)
+(mean 0, variance 1/d; every step but the final multiply is exact in float32,
+and that multiply is correctly rounded on both sides).  A prompt position
+p >= n_sinks carries heavy-hitter keys when its selector word is below
+hh_frac * 2^32 (a Bernoulli draw per position, shared by the sample's KV
+heads); sinks and heavy hitters scale K as above.  Counter words: (pos * d/2 +
+pair, tensor << 8 | head, sample, layer) with tensor 0 = Q, 1 = K, 2 = V, 3 =
+selector; key (seed, 0).
 """
 from __future__ import annotations
 
@@ -231,3 +245,92 @@ def batch_inputs(wl: Workload, device, layer: int = 0, checked=(), sharp: bool =
         k[bi, hk] = torch.from_numpy(uk).to(device=device, dtype=tdt)
         v[bi, hk] = torch.from_numpy(uv).to(device=device, dtype=tdt)
     return q, k, v
+
+
+# ---------------------------------------------------------------------------
+# counter-based stream (Philox4x32-10) for the layer stack
+# ---------------------------------------------------------------------------
+PHILOX_M0, PHILOX_M1 = 0xD2511F53, 0xCD9E8D57      # round multipliers
+PHILOX_W0, PHILOX_W1 = 0x9E3779B9, 0xBB67AE85      # key schedule (Weyl) increments
+T_Q, T_K, T_V, T_SEL = 0, 1, 2, 3
+
+
+def philox4x32_10(ctr: np.ndarray, key: np.ndarray) -> np.ndarray:
+    """Philox4x32 with 10 rounds.  ctr [..., 4] and key [..., 2] (uint32,
+    broadcastable) -> [..., 4] uint32.  A round maps (c0, c1, c2, c3) with
+    (hi0, lo0) = M0 * c0 and (hi1, lo1) = M1 * c2 (64-bit products) to
+    (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0); the key grows by (W0, W1)
+    between rounds."""
+    ctr = np.asarray(ctr, dtype=np.uint32)
+    key = np.asarray(key, dtype=np.uint32)
+    mask = np.uint64(0xFFFFFFFF)
+    c0, c1, c2, c3 = (ctr[..., i].astype(np.uint64) for i in range(4))
+    k0 = key[..., 0].astype(np.uint64)
+    k1 = key[..., 1].astype(np.uint64)
+    for _ in range(10):
+        p0 = c0 * np.uint64(PHILOX_M0)
+        p1 = c2 * np.uint64(PHILOX_M1)
+        c0, c1, c2, c3 = ((p1 >> np.uint64(32)) ^ c1 ^ k0, p1 & mask,
+                          (p0 >> np.uint64(32)) ^ c3 ^ k1, p0 & mask)
+        k0 = (k0 + np.uint64(PHILOX_W0)) & mask
+        k1 = (k1 + np.uint64(PHILOX_W1)) & mask
+    return np.stack([c0, c1, c2, c3], axis=-1).astype(np.uint32)
+
+
+def stack_value_scale(head_dim: int) -> np.float32:
+    """c = float32(sqrt(3) / sqrt(d) / 65536): the Irwin-Hall sum of four 16-bit
+    uniforms has variance 4 * 65536^2 / 12, so (S - mean) * c has variance 1/d."""
+    return np.float32(np.sqrt(3.0) / np.sqrt(head_dim) / 65536.0)
+
+
+def stack_hh_threshold(wl: Workload) -> int:
+    return int(round(wl.hh_frac * 2.0 ** 32)) if wl.hh_mode != "none" else 0
+
+
+def _stack_values(wl: Workload, layer: int, sample: int, tensor: int, head: int,
+                  positions: np.ndarray) -> np.ndarray:
+    """float32 [len(positions), d] elements of one (tensor, head) row range."""
+    d = wl.head_dim
+    pair = np.arange(d // 2, dtype=np.uint64)
+    j = (positions.astype(np.uint64)[:, None] * np.uint64(d // 2) + pair[None, :])
+    ctr = np.zeros(j.shape + (4,), dtype=np.uint32)
+    ctr[..., 0] = j.astype(np.uint32)
+    ctr[..., 1] = (tensor << 8) | head
+    ctr[..., 2] = sample
+    ctr[..., 3] = layer
+    w = philox4x32_10(ctr, np.array([wl.seed, 0], dtype=np.uint32)).astype(np.uint32)  # [T, d/2, 4]
+    lo, hi = w & np.uint32(0xFFFF), w >> np.uint32(16)
+    s0 = lo[..., 0] + hi[..., 0] + lo[..., 1] + hi[..., 1]      # element 2 * pair
+    s1 = lo[..., 2] + hi[..., 2] + lo[..., 3] + hi[..., 3]      # element 2 * pair + 1
+    S = np.stack([s0, s1], axis=-1).reshape(len(positions), d)
+    c = stack_value_scale(d)
+    return (S.astype(np.float32) - np.float32(131070.0)) * c
+
+
+def stack_key_factor(wl: Workload, layer: int, sample: int, positions: np.ndarray) -> np.ndarray:
+    """float32 multiplier of the K row at each position (1, hh_scale or sink_scale)."""
+    positions = np.asarray(positions, dtype=np.int64)
+    ctr = np.zeros(positions.shape + (4,), dtype=np.uint32)
+    ctr[..., 0] = positions.astype(np.uint32)
+    ctr[..., 1] = T_SEL << 8
+    ctr[..., 2] = sample
+    ctr[..., 3] = layer
+    sel = philox4x32_10(ctr, np.array([wl.seed, 0], dtype=np.uint32))[..., 0]
+    f = np.ones(positions.shape, dtype=np.float32)
+    prompt = positions < wl.s
+    heavy = prompt & (positions >= wl.n_sinks) & (sel.astype(np.uint64) < np.uint64(stack_hh_threshold(wl)))
+    f[heavy] = np.float32(wl.hh_scale)
+    f[prompt & (positions < wl.n_sinks)] = np.float32(wl.sink_scale)
+    return f
+
+
+def stack_unit_inputs(wl: Workload, layer: int, sample: int, kv_head: int):
+    """Counter-stream inputs of one unit of the layer stack, float32 arrays exactly
+    representable in wl.dtype: q [G, s+D, d], k [s+D, d], v [s+D, d]."""
+    pos = np.arange(wl.total, dtype=np.int64)
+    G = wl.group
+    k = _stack_values(wl, layer, sample, T_K, kv_head, pos)
+    k = k * stack_key_factor(wl, layer, sample, pos)[:, None]
+    v = _stack_values(wl, layer, sample, T_V, kv_head, pos)
+    q = np.stack([_stack_values(wl, layer, sample, T_Q, kv_head * G + g, pos) for g in range(G)])
+    return (round_to_dtype(q, wl.dtype), round_to_dtype(k, wl.dtype), round_to_dtype(v, wl.dtype))

@@ -172,3 +172,107 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
         if stop_on_failure and st.failures:
             return st
     return st
+
+
+def stack_params(wl: synth.Workload, layer: int, b: int):
+    from paper_2412_05693_amd.batchmax import synth_params
+
+    return synth_params(b=b, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                        dtype=wl.dtype, seed=wl.seed, layer=layer, s=wl.s, hh_frac=wl.hh_frac,
+                        hh_scale=wl.hh_scale, n_sinks=wl.n_sinks, sink_scale=wl.sink_scale,
+                        heavy=wl.hh_mode != "none")
+
+
+def run_stack_parity(wl: synth.Workload, checked, *, device="cuda", decode_steps=None,
+                     stop_on_failure=True) -> Stats:
+    """The layer stack: every layer's inputs come from the device generator one
+    block (or decode row) at a time; the checked units ``(layer, sample,
+    kv_head)`` are compared with the oracle fed by the host evaluation of the
+    same counter-based stream."""
+    from paper_2412_05693_amd.batchmax import PDStack, synth_qkv
+
+    st = Stats()
+    b, H, Hk, d, B, G = wl.b, wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.block, wl.group
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    stack = PDStack(n_layers=wl.n_layers, b=b, s=wl.s, kv_max=wl.kv_max, block=B,
+                    max_gen=wl.n_decode, n_heads=H, n_kv_heads=Hk, head_dim=d, dtype=wl.dtype,
+                    sm_scale=wl.sm_scale, device=device)
+    stack.reset()
+    q = torch.empty((b, H, B, d), dtype=tdt, device=device)
+    k = torch.empty((b, Hk, B, d), dtype=tdt, device=device)
+    v = torch.empty_like(k)
+    o = torch.zeros_like(q)
+    qd = torch.empty((b, H, 1, d), dtype=tdt, device=device)
+    kd = torch.empty((b, Hk, 1, d), dtype=tdt, device=device)
+    vd = torch.empty_like(kd)
+    od = torch.zeros_like(qd)
+    params = [stack_params(wl, layer, b) for layer in range(wl.n_layers)]
+    by_layer = {}
+    for (layer, bi, hk) in checked:
+        by_layer.setdefault(layer, []).append((bi, hk))
+    uin = {u: synth.stack_unit_inputs(wl, *u) for u in checked}
+    orcs = {u: opd.StepOracle(head_dim=d, group=G, kv_max=wl.kv_max, sm_scale=wl.sm_scale)
+            for u in checked}
+    tol = OUT_TOL[wl.dtype]
+    D = wl.n_decode if decode_steps is None else decode_steps
+
+    def check_out(tag, out, u, n, ref):
+        _, bi, hk = u
+        got = out[bi, hk * G:(hk + 1) * G, :n].float().cpu().numpy().astype(np.float64)
+        err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+        st.max_out_err = max(st.max_out_err, err)
+        if not err <= tol:
+            st.fail(f"{tag} unit {u}: output error {err:.3e} > {tol}")
+
+    for t0 in range(0, wl.s, B):
+        n = min(B, wl.s - t0)
+        for layer in range(wl.n_layers):
+            pd = stack.layers[layer]
+            synth_qkv(params[layer], t0, q, k, v)
+            pd.prefill_block(t0, n, q, k, v, o, row=0)
+            units = by_layer.get(layer)
+            if units:
+                length = pd.length
+                pos, score, dlen = _snapshot(pd, units, length)
+                for i, (bi, hk) in enumerate(units):
+                    u = (layer, bi, hk)
+                    uq, uk, uv = uin[u]
+                    ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
+                    check_out(f"block {t0}", o, u, n, ref)
+                    _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i],
+                                   length, st)
+            pd.evict_compact(t0 + n - 1)
+            if units:
+                length = pd.length
+                pos, score, dlen = _snapshot(pd, units, length)
+                for i, (bi, hk) in enumerate(units):
+                    u = (layer, bi, hk)
+                    ev = orcs[u].evict(t0 + n - 1, "prefill")
+                    _compare_cut(f"cut {t0 + n - 1} unit {u}", orcs[u], ev, pos[i], st)
+                    _compare_state(f"cut {t0 + n - 1} unit {u}", orcs[u], pos[i], score[i],
+                                   dlen[i], length, st)
+        if stop_on_failure and st.failures:
+            return st
+
+    for t in range(D):
+        p = wl.s + t
+        for layer in range(wl.n_layers):
+            pd = stack.layers[layer]
+            synth_qkv(params[layer], p, qd, kd, vd)
+            pd.decode_step(p, qd, kd, vd, od, row=0)
+            units = by_layer.get(layer)
+            if units:
+                length = pd.length
+                pos, score, dlen = _snapshot(pd, units, length)
+                for i, (bi, hk) in enumerate(units):
+                    u = (layer, bi, hk)
+                    uq, uk, uv = uin[u]
+                    ref, ev = orcs[u].decode_step(p, uq[:, p], uk[p], uv[p])
+                    check_out(f"decode {p}", od, u, 1, ref[:, None, :])
+                    _compare_cut(f"decode {p} unit {u}", orcs[u], ev, pos[i], st)
+                    _compare_state(f"decode {p} unit {u}", orcs[u], pos[i], score[i], dlen[i],
+                                   length, st)
+        if stop_on_failure and st.failures:
+            return st
+    stack.close()
+    return st

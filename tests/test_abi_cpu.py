@@ -37,8 +37,10 @@ def status_of(fn, *args):
 
 
 def test_header_symbols_exported():
-    text = open(HEADER).read()
-    declared = sorted(set(re.findall(r"\b(bm_[a-z_]+)\s*\(", text)))
+    inc = os.path.join(ROOT, "include")
+    text = "".join(open(os.path.join(inc, f)).read() for f in sorted(os.listdir(inc))
+                   if f.endswith(".h"))
+    declared = sorted(set(re.findall(r"\b(bm_[a-z0-9_]+)\s*\(", text)))
     assert declared, "no declarations found"
     lib = ctypes.CDLL(bmx.LIB_PATH)
     for name in declared:
@@ -192,3 +194,22 @@ def test_algorithmic_work_figures():
     by = bmx.decode_bytes_per_step(b=64, n_kv_heads=8, group=4, head_dim=128, kv_max=512,
                                    elem_bytes=2)
     assert by == 512 * 271368
+
+
+def test_synth_argument_checks():
+    # every check runs on the host before a launch, so fake pointers are safe
+    mk = lambda **kw: bmx.synth_params(**{**dict(b=2, n_heads=8, n_kv_heads=2, head_dim=64,
+                                                 dtype="bf16", seed=1, layer=0, s=64), **kw})
+    p = mk()
+    call = lambda prm, t0, n, q, k, v, ld: status_of(bmx.bm_synth_qkv, prm, t0, n, q, k, v, ld, 0)
+    bad = bmx.BM_ERR_INVALID_ARG
+    assert call(p, 0, 0, FAKE, FAKE, FAKE, 1) == bad          # no rows
+    assert call(p, -1, 4, FAKE, FAKE, FAKE, 4) == bad         # negative position
+    assert call(p, 0, 4, FAKE, FAKE, FAKE, 3) == bad          # seq_ld < rows
+    assert call(p, 0, 4, 0, FAKE, FAKE, 4) == bad             # null q
+    assert call(p, 0, 4, FAKE + 2, FAKE, FAKE, 4) == bad      # misaligned q
+    assert call(mk(head_dim=63), 0, 4, FAKE, FAKE, FAKE, 4) == bad
+    assert call(mk(dtype=7), 0, 4, FAKE, FAKE, FAKE, 4) == bad
+    assert call(mk(b=0), 0, 4, FAKE, FAKE, FAKE, 4) == bad
+    assert status_of(bmx.bm_philox4x32_10, FAKE, FAKE, 0, 0) == bad
+    assert status_of(bmx.bm_philox4x32_10, 0, FAKE, 4, 0) == bad

@@ -39,7 +39,7 @@ typedef struct bm_synth {
   int32_t b;             /* samples                                        */
   int32_t n_heads;       /* query heads                                    */
   int32_t n_kv_heads;    /* KV heads                                       */
-  int32_t head_dim;      /* even                                           */
+  int32_t head_dim;      /* twice a power of two                           */
   int32_t dtype;         /* bm_dtype: 0 float32, 1 bfloat16                */
   uint32_t seed;         /* key word 0                                     */
   int32_t layer;         /* counter word 3                                 */

@@ -348,8 +348,10 @@ BM_EXPORT int bm_synth_qkv(const bm_synth* p, int32_t t0, int32_t n_rows, void* 
                            void* v, int32_t seq_ld, hipStream_t stream) {
   if (!p) return fail(BM_ERR_INVALID_ARG, "params are null");
   if (!q || !k || !v) return fail(BM_ERR_INVALID_ARG, "q, k or v is null");
-  if (p->b < 1 || p->n_heads < 1 || p->n_kv_heads < 1 || p->head_dim < 2 || (p->head_dim & 1))
-    return fail(BM_ERR_INVALID_ARG, "b, heads must be positive and head_dim even");
+  const int half = p->head_dim / 2;
+  if (p->b < 1 || p->n_heads < 1 || p->n_kv_heads < 1 || p->head_dim < 2 || (p->head_dim & 1) ||
+      (half & (half - 1)))
+    return fail(BM_ERR_INVALID_ARG, "b, heads must be positive and head_dim / 2 a power of two");
   if (p->dtype != BM_F32 && p->dtype != BM_BF16)
     return fail(BM_ERR_INVALID_ARG, "dtype %d is neither BM_F32 nor BM_BF16", p->dtype);
   if (t0 < 0 || n_rows < 1 || seq_ld < n_rows)

@@ -4,8 +4,8 @@
 // mapping (c0, c1, c2, c3) with the 64-bit products M0 * c0 = (hi0, lo0) and
 // M1 * c2 = (hi1, lo1) to (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0), the key
 // growing by the Weyl constants (W0, W1) between rounds.  One call yields two
-// elements (Irwin-Hall sums of four 16-bit uniforms, see bm_synth.h); threads
-// walk the elements pair by pair so every store is 4 or 8 contiguous bytes.
+// elements (Irwin-Hall sums of four 16-bit uniforms, see bm_synth.h); a thread
+// owns one element pair, so every store is 4 or 8 contiguous bytes.
 #include "bm_internal.h"
 
 namespace bm {
@@ -30,56 +30,53 @@ __device__ __forceinline__ uint32_t ih4(uint32_t a, uint32_t b) {
   return (a & 0xFFFFu) + (a >> 16) + (b & 0xFFFFu) + (b >> 16);
 }
 
+// One block covers 256 element pairs of one (sample, Q/K/V head) row range;
+// all index arithmetic is 32-bit (pairs per row is a power of two).
 template <bool BF16>
-__global__ void __launch_bounds__(256) synth_qkv_kernel(SynthArgs a) {
-  const int P = a.head_dim / 2;                       // element pairs per row
+__global__ void __launch_bounds__(256) synth_qkv_kernel(SynthArgs a, int chunks, int pshift) {
+  const int P = 1 << pshift;                          // element pairs per row (d / 2)
   const int HT = a.n_heads + 2 * a.n_kv_heads;        // rows of Q, K, V heads
-  const int64_t total = (int64_t)a.b * HT * a.n_rows * P;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; it < total; it += stride) {
-    const int pair = (int)(it % P);
-    int64_t rest = it / P;
-    const int r = (int)(rest % a.n_rows);
-    rest /= a.n_rows;
-    const int ht = (int)(rest % HT);
-    const int sample = (int)(rest / HT);
-    int tensor, head, nh;
-    void* base;
-    if (ht < a.n_heads) {
-      tensor = 0; head = ht; nh = a.n_heads; base = a.q;
-    } else if (ht < a.n_heads + a.n_kv_heads) {
-      tensor = 1; head = ht - a.n_heads; nh = a.n_kv_heads; base = a.k;
+  const int blk = blockIdx.x;
+  const int chunk = blk % chunks;
+  const int sh = blk / chunks;                        // sample * HT + ht
+  const int ht = sh % HT, sample = sh / HT;
+  const int local = chunk * 256 + threadIdx.x;
+  const int r = local >> pshift, pair = local & (P - 1);
+  if (r >= a.n_rows) return;
+  int tensor, head, nh;
+  void* base;
+  if (ht < a.n_heads) {
+    tensor = 0; head = ht; nh = a.n_heads; base = a.q;
+  } else if (ht < a.n_heads + a.n_kv_heads) {
+    tensor = 1; head = ht - a.n_heads; nh = a.n_kv_heads; base = a.k;
+  } else {
+    tensor = 2; head = ht - a.n_heads - a.n_kv_heads; nh = a.n_kv_heads; base = a.v;
+  }
+  const uint32_t pos = (uint32_t)(a.t0 + r);
+  const uint4 w = philox4x32_10(
+      make_uint4(pos * (uint32_t)P + (uint32_t)pair, ((uint32_t)tensor << 8) | (uint32_t)head,
+                 (uint32_t)sample, (uint32_t)a.layer),
+      a.seed, 0u);
+  float z0 = ((float)ih4(w.x, w.y) - 131070.0f) * a.value_scale;
+  float z1 = ((float)ih4(w.z, w.w) - 131070.0f) * a.value_scale;
+  if (tensor == 1 && (int)pos < a.s) {
+    float f = 1.0f;
+    if ((int)pos < a.n_sinks) {
+      f = a.sink_scale;
     } else {
-      tensor = 2; head = ht - a.n_heads - a.n_kv_heads; nh = a.n_kv_heads; base = a.v;
+      const uint4 sel = philox4x32_10(make_uint4(pos, 3u << 8, (uint32_t)sample, (uint32_t)a.layer),
+                                      a.seed, 0u);
+      if (sel.x < a.hh_threshold) f = a.hh_scale;
     }
-    const uint32_t pos = (uint32_t)(a.t0 + r);
-    const uint4 w = philox4x32_10(
-        make_uint4(pos * (uint32_t)P + (uint32_t)pair, ((uint32_t)tensor << 8) | (uint32_t)head,
-                   (uint32_t)sample, (uint32_t)a.layer),
-        a.seed, 0u);
-    float z0 = ((float)ih4(w.x, w.y) - 131070.0f) * a.value_scale;
-    float z1 = ((float)ih4(w.z, w.w) - 131070.0f) * a.value_scale;
-    if (tensor == 1 && (int)pos < a.s) {
-      float f = 1.0f;
-      if ((int)pos < a.n_sinks) {
-        f = a.sink_scale;
-      } else {
-        const uint4 sel = philox4x32_10(make_uint4(pos, 3u << 8, (uint32_t)sample, (uint32_t)a.layer),
-                                        a.seed, 0u);
-        if (sel.x < a.hh_threshold) f = a.hh_scale;
-      }
-      z0 *= f;
-      z1 *= f;
-    }
-    const int64_t off = (((int64_t)sample * nh + head) * a.seq_ld + r) * a.head_dim + 2 * pair;
-    if constexpr (BF16) {
-      __bf16* dst = static_cast<__bf16*>(base) + off;
-      typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-      *reinterpret_cast<bf16x2*>(dst) = bf16x2{(__bf16)z0, (__bf16)z1};
-    } else {
-      float* dst = static_cast<float*>(base) + off;
-      *reinterpret_cast<float2*>(dst) = make_float2(z0, z1);
-    }
+    z0 *= f;
+    z1 *= f;
+  }
+  const int64_t off = (((int64_t)sample * nh + head) * a.seq_ld + r) * (2 * P) + 2 * pair;
+  if constexpr (BF16) {
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+    *reinterpret_cast<bf16x2*>(static_cast<__bf16*>(base) + off) = bf16x2{(__bf16)z0, (__bf16)z1};
+  } else {
+    *reinterpret_cast<float2*>(static_cast<float*>(base) + off) = make_float2(z0, z1);
   }
 }
 
@@ -105,11 +102,18 @@ unsigned grid_for(int64_t items) {
 }  // namespace
 
 hipError_t launch_synth_qkv(const SynthArgs& a, hipStream_t stream) {
-  const int64_t items = (int64_t)a.b * (a.n_heads + 2 * a.n_kv_heads) * a.n_rows * (a.head_dim / 2);
+  int pshift = 0;
+  while ((1 << pshift) < a.head_dim / 2) ++pshift;
+  if ((1 << pshift) != a.head_dim / 2) return hipErrorInvalidValue;   // d / 2 a power of two
+  const int64_t chunks = ((int64_t)a.n_rows * (a.head_dim / 2) + 255) / 256;
+  const int64_t blocks = (int64_t)a.b * (a.n_heads + 2 * a.n_kv_heads) * chunks;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
   if (a.dtype == BM_BF16)
-    hipLaunchKernelGGL(synth_qkv_kernel<true>, dim3(grid_for(items)), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(synth_qkv_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, a,
+                       (int)chunks, pshift);
   else
-    hipLaunchKernelGGL(synth_qkv_kernel<false>, dim3(grid_for(items)), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(synth_qkv_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, a,
+                       (int)chunks, pshift);
   return hipGetLastError();
 }
 

@@ -112,9 +112,13 @@ def _oracle_unit(args):
 
 
 def cpu_baseline(name, overrides, budget_s):
+    """Time the oracle on a sample of units (one per process).  Returns the
+    measurement; ``cpu_baseline_line`` scales it to the workload that ran."""
     from paper_2412_05693_amd import synth
 
     wl = synth.WORKLOADS[name].with_(**overrides)
+    if wl.b == 0:                     # the stack's batch is planned on the GPU later;
+        wl = wl.with_(b=64)           # a unit's oracle cost does not depend on b
     cores = len(os.sched_getaffinity(0))
     cores = max(1, min(cores, 16))
     for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
@@ -125,31 +129,35 @@ def cpu_baseline(name, overrides, budget_s):
         units = [((i * 7919) % wl.n_layers, bi, hk) for i, (bi, hk) in enumerate(units)]
     else:
         units = [(0, bi, hk) for (bi, hk) in units]
-    total_units = wl.units * wl.n_layers
-    done, t0 = 0, time.perf_counter()
-    unit_s = 0.0
+    ov = dict(overrides, b=wl.b)
+    t0 = time.perf_counter()
     with ctx.Pool(cores) as pool:
         # first wave sizes the sample: keep to about budget_s of wall time
-        first = pool.map(_oracle_unit, [(name, overrides) + u for u in units[:cores]])
+        first = pool.map(_oracle_unit, [(name, ov) + u for u in units[:cores]])
         per_unit = sum(first) / len(first)
         want = max(cores, int(budget_s * cores / max(per_unit, 1e-6)))
         want = min(want, len(units))
         rest = units[cores:want]
-        more = pool.map(_oracle_unit, [(name, overrides) + u for u in rest]) if rest else []
-        done = cores + len(rest)
-        unit_s = sum(first) + sum(more)
-    wall = time.perf_counter() - t0
-    # units are independent and equal in cost: the oracle time of the whole
-    # workload is the sampled units' oracle time scaled to all units, spread
-    # over the same number of processes
-    t_full = unit_s / done * total_units / cores
+        more = pool.map(_oracle_unit, [(name, ov) + u for u in rest]) if rest else []
+    done = cores + len(rest)
+    unit_s = sum(first) + sum(more)
+    return {"per_unit_s": unit_s / done, "cores": cores, "done": done, "unit_s": unit_s,
+            "wall": time.perf_counter() - t0, "n_layers": wl.n_layers}
+
+
+def cpu_baseline_line(m, wl):
+    """The oracle's throughput on the workload that ran: units are independent
+    and equal in cost, so its time is the sampled units' mean oracle time times
+    all units, spread over the same number of processes."""
+    total_units = wl.units * wl.n_layers
+    t_full = m["per_unit_s"] * total_units / m["cores"]
     tok = wl.b * (wl.s + wl.n_decode)
     what = "(layer, sample, KV head)" if wl.n_layers > 1 else "(sample, KV head)"
-    return {"value": tok / t_full, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} of {total_units} {what} units of {wl.name} (b={wl.b}), full P&D "
-                      f"each, float64 numpy, one unit per process and one BLAS thread; "
-                      f"{unit_s:.1f} s of oracle time in {wall:.1f} s wall, scaled to all "
-                      f"units over {cores} processes"}
+    return {"value": tok / t_full, "unit": "tokens/s", "cores": m["cores"], "kind": "oracle",
+            "sample": f"{m['done']} {what} units of {wl.name}, full P&D each, float64 numpy, "
+                      f"one unit per process and one BLAS thread; {m['unit_s']:.1f} s of oracle "
+                      f"time in {m['wall']:.1f} s wall, scaled to all {total_units} units of "
+                      f"b={wl.b} over {m['cores']} processes"}
 
 
 # ---------------------------------------------------------------------------
@@ -455,7 +463,7 @@ def main():
                    "kv_max": wl.kv_max, "block": wl.block, "decode_steps": wl.n_decode,
                    "parallelism": "single GPU"},
         "roofline": res["roofline"],
-        "cpu_baseline": cpu,
+        "cpu_baseline": cpu_baseline_line(cpu, wl) if cpu else None,
         "kernels": res["kernels"],
         "phases": res["phases"],
     }

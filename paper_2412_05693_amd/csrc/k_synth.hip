@@ -13,6 +13,7 @@ namespace {
 
 constexpr uint32_t kM0 = 0xD2511F53u, kM1 = 0xCD9E8D57u;
 constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;
+constexpr int64_t kMaxGrid = 1 << 20;   // workgroups per launch (2^28 work-items)
 
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
@@ -30,19 +31,20 @@ __device__ __forceinline__ uint32_t ih4(uint32_t a, uint32_t b) {
   return (a & 0xFFFFu) + (a >> 16) + (b & 0xFFFFu) + (b >> 16);
 }
 
-// One block covers 256 element pairs of one (sample, Q/K/V head) row range;
-// all index arithmetic is 32-bit (pairs per row is a power of two).
+// A virtual block covers 256 element pairs of one (sample, Q/K/V head) row
+// range; workgroups stride over the virtual blocks, so a launch never needs
+// more than kMaxGrid workgroups.  All index arithmetic is 32-bit (pairs per
+// row is a power of two).
 template <bool BF16>
-__global__ void __launch_bounds__(256) synth_qkv_kernel(SynthArgs a, int chunks, int pshift) {
+__device__ __forceinline__ void synth_block(const SynthArgs& a, int chunks, int pshift, int blk) {
   const int P = 1 << pshift;                          // element pairs per row (d / 2)
   const int HT = a.n_heads + 2 * a.n_kv_heads;        // rows of Q, K, V heads
-  const int blk = blockIdx.x;
   const int chunk = blk % chunks;
   const int sh = blk / chunks;                        // sample * HT + ht
   const int ht = sh % HT, sample = sh / HT;
   const int local = chunk * 256 + threadIdx.x;
   const int r = local >> pshift, pair = local & (P - 1);
-  if (r >= a.n_rows) return;
+  if (r >= a.n_rows) return;   // past the last row of the range: no pair for this thread
   int tensor, head, nh;
   void* base;
   if (ht < a.n_heads) {
@@ -80,6 +82,13 @@ __global__ void __launch_bounds__(256) synth_qkv_kernel(SynthArgs a, int chunks,
   }
 }
 
+template <bool BF16>
+__global__ void __launch_bounds__(256) synth_qkv_kernel(SynthArgs a, int chunks, int pshift,
+                                                        int blocks) {
+  for (int blk = blockIdx.x; blk < blocks; blk += gridDim.x)
+    synth_block<BF16>(a, chunks, pshift, blk);
+}
+
 __global__ void __launch_bounds__(256) philox_kernel(const uint32_t* in, uint32_t* out, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
@@ -108,12 +117,13 @@ hipError_t launch_synth_qkv(const SynthArgs& a, hipStream_t stream) {
   const int64_t chunks = ((int64_t)a.n_rows * (a.head_dim / 2) + 255) / 256;
   const int64_t blocks = (int64_t)a.b * (a.n_heads + 2 * a.n_kv_heads) * chunks;
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)(blocks < kMaxGrid ? blocks : kMaxGrid);
   if (a.dtype == BM_BF16)
-    hipLaunchKernelGGL(synth_qkv_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, a,
-                       (int)chunks, pshift);
+    hipLaunchKernelGGL(synth_qkv_kernel<true>, dim3(grid), dim3(256), 0, stream, a, (int)chunks,
+                       pshift, (int)blocks);
   else
-    hipLaunchKernelGGL(synth_qkv_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, a,
-                       (int)chunks, pshift);
+    hipLaunchKernelGGL(synth_qkv_kernel<false>, dim3(grid), dim3(256), 0, stream, a, (int)chunks,
+                       pshift, (int)blocks);
   return hipGetLastError();
 }
 

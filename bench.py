@@ -54,10 +54,11 @@ def source_digest() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, units: int = 0):
     """HBM bytes per prefill launch from a committed counter record
     (`traffic-record:` line under profiles/), or None when there is none for
-    this workload or the kernel sources changed since it was taken."""
+    this workload or the kernel sources changed since it was taken.  A record
+    given per unit is scaled by the launch's unit count."""
     pdir = os.path.join(ROOT, "profiles")
     if not os.path.isdir(pdir):
         return None
@@ -72,7 +73,10 @@ def measured_traffic(workload: str):
                     continue
                 kv = dict(item.split("=", 1) for item in line.split()[1:] if "=" in item)
                 if kv.get("workload") == workload and kv.get("source_sha256") == digest:
-                    return int(kv["bytes_per_launch"])
+                    if "bytes_per_launch" in kv:
+                        return int(kv["bytes_per_launch"])
+                    if "bytes_per_unit" in kv and units:
+                        return int(kv["bytes_per_unit"]) * units
     return None
 
 
@@ -382,10 +386,13 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd_ = kernels[dom]
-    traffic = measured_traffic(wl.name) if dom == "prefill_attention" else None
+    traffic = measured_traffic(wl.name, b * Hk) if dom == "prefill_attention" else None
     roofline = {"bound": kd_["bound"], "achieved": round(kd_["achieved"], 3), "peak": kd_["peak"],
                 "unit": kd_["unit"], "frac": round(kd_["frac"], 5), "traffic": traffic,
                 "kernel": dom}
+    if traffic is not None:
+        roofline["traffic_basis"] = ("FETCH_SIZE/WRITE_SIZE per unit of the same launches "
+                                     "measured on c2, scaled to this launch's units")
     tokens = b * (wl.s + wl.n_decode)
     stack.close()
     return {

@@ -59,6 +59,18 @@ __device__ __forceinline__ int kappa(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
+// x of lane i combined with x of lane i ^ 32 through gfx950's cross-half swap
+// (no LDS round trip); the swap returns the two values in the same order on
+// both lanes, so both get bit-identical results
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   bf16x2 r = {(__bf16)lo, (__bf16)hi};
   return __builtin_bit_cast(uint32_t, r);
@@ -314,6 +326,17 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         acc[st] = ST ? mfma_step<BF16, D>(kf[kk & 1][st], qf[kk], acc[st])
                      : mfma_step<BF16, D>(qf[kk], kf[kk & 1][st], acc[st]);
     }
+    if constexpr (BF16) {
+      // pin the order: the reads of step kk + 1 go out before the MFMAs of
+      // step kk (left alone, the scheduler sinks each read to its MFMA)
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);   // DS reads
+#pragma unroll
+      for (int kk = 0; kk + 2 < C::QSTEPS; ++kk) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0); // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    }
   };
   auto qk_st = [&](const char* ks, f32x16* acc) __device__ { qk_tile(std::true_type{}, ks, acc); };
   auto qk_s = [&](const char* ks, f32x16* acc) __device__ { qk_tile(std::false_type{}, ks, acc); };
@@ -342,7 +365,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[st][r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    tmax = xhalf_max(tmax);
     // The reference m_run moves only when some row of the wave sees a logit
     // more than kRescaleLog2 above it: the probabilities stay below
     // 2^kRescaleLog2 (exact in fp32, fine in bf16) and the O rescale is rare.
@@ -460,7 +483,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   }
 
   // ---- finish rows: normalise, store O, row log-sum-exp (log2 units) ----
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = xhalf_sum(l_run);
   float lse2 = kPosInf;
   if (s.wave_active) {
     const float inv = 1.0f / l_tot;
@@ -509,7 +532,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         }
         csum += __builtin_amdgcn_exp2f(x);
       }
-      csum += __shfl_xor(csum, 32);
+      csum = xhalf_sum(csum);
       if (s.h == 0) cs[s.w][key] = csum;
     }
   };

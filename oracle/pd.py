@@ -128,23 +128,26 @@ class UnitOracle:
         """
         return self.score / (curr_id + 1 - self.pos).astype(np.float64)
 
-    def evict(self, curr_id: int, kind: str) -> EvictionEvent | None:
-        """Cut the cache back to ``kv_max`` entries (Sec. 3.1; Sec. 3.2 rule).
+    def evict(self, curr_id: int, kind: str, target: int | None = None) -> EvictionEvent | None:
+        """Cut the cache back to ``target`` (default ``kv_max``) entries (Sec. 3.1;
+        Sec. 3.2 rule).
 
         The entries with the smallest ``ave_weights`` are removed; on an exact
         tie the older entry (smaller position) goes first (reading R8).  No-op
-        while the cache holds at most ``kv_max`` entries (reading R16).
+        while the cache holds at most ``target`` entries (reading R16).
         Survivors keep their accumulated scores (reading R13).
         """
+        target = self.kv_max if target is None else target
         n = self.n
-        if n <= self.kv_max:
+        if n <= target:
             return None
         ave = self.averages(curr_id)
         order = np.lexsort((self.pos, ave))        # ascending ave, then ascending pos
-        n_evict = n - self.kv_max
+        n_evict = n - target
         evict_idx = order[:n_evict]
         keep_idx = np.sort(order[n_evict:])
-        gap = float(ave[order[n_evict]] - ave[order[n_evict - 1]])
+        # smallest kept average minus largest removed one (no tie when nothing is kept)
+        gap = float(ave[order[n_evict]] - ave[order[n_evict - 1]]) if n_evict < n else np.inf
         by_pos = np.argsort(self.pos)
         ev = EvictionEvent(
             kind=kind, curr_id=int(curr_id), n_before=n,
@@ -182,22 +185,40 @@ class UnitOracle:
         o = self.attend(np.asarray(q)[:, None, :], pos)[:, 0, :]
         return o, self.evict(pos, "decode")
 
+    def decode_step_alg1(self, pos: int, q: np.ndarray, k: np.ndarray, v: np.ndarray, p: int):
+        """One decode step of Algorithm 1's decoding loop taken literally: when
+        the cache holds ``kv_max`` entries, first remove ``p`` of them (ranked
+        with ``curr_id = pos - 1``, the last processed position, reading R4),
+        then process the token at ``pos`` (append and attend, no removal).
+        Returns (outputs ``[G, d]``, event or None)."""
+        ev = None
+        if self.n == self.kv_max:
+            ev = self.evict(pos - 1, "decode", target=self.kv_max - p)
+        self.append(pos, np.asarray(k)[None], np.asarray(v)[None])
+        o = self.attend(np.asarray(q)[:, None, :], pos)[:, 0, :]
+        return o, ev
+
 
 class StepOracle(UnitOracle):
     """``UnitOracle`` that remembers the entries of its last cut, so that a
     comparison harness can adopt another valid kept set after a near-tie."""
 
-    def evict(self, curr_id: int, kind: str):
+    def evict(self, curr_id: int, kind: str, target: int | None = None):
         before = (self.pos.copy(), self.k.copy(), self.v.copy(), self.score.copy(),
                   self.evicted_score_total)
-        ev = super().evict(curr_id, kind)
+        ev = super().evict(curr_id, kind, target)
         self._last = before if ev is not None else None
+        self._last_target = self.kv_max if target is None else target
         return ev
 
     def adopt(self, kept_pos) -> None:
+        """Replace the result of the last cut by another kept set of the same size.
+        Call it right after that cut (before anything is appended)."""
         pos, k, v, score, evt = self._last
         kept_pos = np.asarray(sorted(int(p) for p in kept_pos), dtype=np.int64)
-        if kept_pos.shape[0] != self.kv_max:
+        size = getattr(self, "_last_target", None)
+        size = self.kv_max if size is None else size
+        if kept_pos.shape[0] != size:
             raise ValueError("adopted kept set has the wrong size")
         idx = np.searchsorted(pos[np.argsort(pos)], kept_pos)
         order = np.argsort(pos)
@@ -223,7 +244,7 @@ class Trace:
 
 
 def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
-             sm_scale: float) -> Trace:
+             sm_scale: float, p_dec: int = 0) -> Trace:
     """Full P&D run of one unit (Sec. 3.1, Algorithm 1 under reading R1).
 
     ``q`` is ``[G, s + n_decode, d]``; ``k``, ``v`` are ``[s + n_decode, d]``,
@@ -231,7 +252,9 @@ def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
     the vectors of every position are given).  Prefill: for t0 = 0, block, ...
     process [t0, t1) with t1 = min(s, t0 + block) (reading R17), then cut with
     curr_id = t1 - 1.  Decode: step t processes position s + t (reading R12)
-    and cuts with curr_id = s + t.
+    and cuts with curr_id = s + t; with ``p_dec > 0`` it follows Algorithm 1's
+    decoding loop literally instead (``decode_step_alg1``: remove ``p_dec``
+    entries when the cache is full, before the token is processed).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -250,7 +273,10 @@ def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
         t0 = t1
     for t in range(n_decode):
         i = s + t
-        out[:, i], ev = unit.decode_step(i, q[:, i], k[i], v[i])
+        if p_dec > 0:
+            out[:, i], ev = unit.decode_step_alg1(i, q[:, i], k[i], v[i], p_dec)
+        else:
+            out[:, i], ev = unit.decode_step(i, q[:, i], k[i], v[i])
         if ev is not None:
             events.append(ev)
     order = np.argsort(unit.pos)

@@ -436,3 +436,64 @@ def test_planted_mistake_is_caught(mutant):
         except (ValueError, IndexError):
             failures += 1
     assert failures >= 1, f"no pin catches {mutant.__name__}"
+
+
+# --- Algorithm 1's decoding loop taken literally (remove p when full) ----------
+def _alg1_inputs(seed, G=2, T=48, d=16):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((G, T, d)) / np.sqrt(d)
+    k = rng.standard_normal((T, d)) / np.sqrt(d)
+    v = rng.standard_normal((T, d))
+    return q, k, v
+
+
+@pytest.mark.parametrize("p", [1, 3, 8])
+def test_alg1_decode_lengths_and_removal_rule(p):
+    # lengths: full (kv_max) when a step starts -> remove p first, then append;
+    # every removal takes the p smallest (ave, pos) with curr_id = pos - 1
+    q, k, v = _alg1_inputs(5 + p)
+    s, kv, B, D = 16, 8, 4, 32
+    unit = opd.UnitOracle(head_dim=16, group=2, kv_max=kv, sm_scale=0.25)
+    for t0 in range(0, s, B):
+        unit.prefill_block(t0, q[:, t0:t0 + B], k[t0:t0 + B], v[t0:t0 + B])
+        unit.evict(t0 + B - 1, "prefill")
+    assert unit.n == kv
+    cuts = 0
+    for t in range(D):
+        i = s + t
+        full = unit.n == kv
+        _, ev = unit.decode_step_alg1(i, q[:, i], k[i], v[i], p)
+        assert (ev is not None) == full
+        if ev is not None:
+            cuts += 1
+            assert ev.curr_id == i - 1 and ev.n_before == kv
+            pairs = sorted(zip(ev.all_ave, ev.all_pos))
+            assert sorted(int(x) for x in ev.evicted_pos) == sorted(int(b) for _, b in pairs[:p])
+            # the averages come from the scores and ages at curr_id = i - 1
+            assert np.allclose(ev.all_ave, ev.all_score / (i - ev.all_pos))
+        assert unit.n == (kv - p + 1 if full else min(kv, unit.n))
+        assert unit.n <= kv
+    assert cuts == len(range(0, D, p)) if p > 1 else cuts == D
+
+
+def test_alg1_decode_removing_everything_leaves_the_new_token():
+    # p = kv_max: the cut empties the cache, so the new token attends to itself
+    # alone and its output is exactly its own value row
+    q, k, v = _alg1_inputs(3)
+    s, kv, B = 16, 8, 8
+    unit = opd.UnitOracle(head_dim=16, group=2, kv_max=kv, sm_scale=0.25)
+    for t0 in range(0, s, B):
+        unit.prefill_block(t0, q[:, t0:t0 + B], k[t0:t0 + B], v[t0:t0 + B])
+        unit.evict(t0 + B - 1, "prefill")
+    o, ev = unit.decode_step_alg1(s, q[:, s], k[s], v[s], kv)
+    assert ev is not None and len(ev.kept_pos) == 0
+    assert np.array_equal(o, np.broadcast_to(v[s], o.shape))
+    assert np.allclose(unit.score, [2.0])       # both heads put weight 1 on it
+
+
+def test_alg1_decode_matches_dense_when_bound_is_never_reached():
+    q, k, v = _alg1_inputs(9)
+    s, D = 16, 32
+    a = opd.run_unit(q, k, v, s=s, kv_max=64, block=4, n_decode=D, sm_scale=0.25)
+    b = opd.run_unit(q, k, v, s=s, kv_max=64, block=4, n_decode=D, sm_scale=0.25, p_dec=5)
+    assert np.array_equal(a.out, b.out) and not b.events

@@ -111,7 +111,7 @@ def _oracle_unit(args):
     with threadpool_limits(1):     # one unit per process, one BLAS thread each
         t = time.perf_counter()
         opd.run_unit(q, k, v, s=wl.s, kv_max=wl.kv_max, block=wl.block, n_decode=wl.n_decode,
-                     sm_scale=wl.sm_scale)
+                     sm_scale=wl.sm_scale, p_dec=wl.decode_p)
         return time.perf_counter() - t
 
 
@@ -167,6 +167,18 @@ def cpu_baseline_line(m, wl):
 # ---------------------------------------------------------------------------
 # GPU run
 # ---------------------------------------------------------------------------
+def decode_bytes(bmx, wl, b):
+    """Algorithmic HBM bytes of all decode launches of one layer: each step at
+    the cache length its attention reads (the removal launches of the p > 0
+    schedule run inside the timed decode phase but add no bytes here)."""
+    es = 4 if wl.dtype == "f32" else 2
+    lens = bmx.decode_cache_lengths(s=wl.s, kv_max=wl.kv_max, n_decode=wl.n_decode,
+                                    p=wl.decode_p)
+    return sum(bmx.decode_bytes_per_step(b=b, n_kv_heads=wl.n_kv_heads, group=wl.group,
+                                         head_dim=wl.head_dim, kv_max=n, elem_bytes=es)
+               for n in lens)
+
+
 def gpu_bench(name, overrides, steps, warmup):
     import torch
 
@@ -181,6 +193,7 @@ def gpu_bench(name, overrides, steps, warmup):
     pd = bmx.PDAttention(b=wl.b, s=wl.s, kv_max=wl.kv_max, block=wl.block, max_gen=wl.n_decode,
                          n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
                          dtype=wl.dtype, sm_scale=wl.sm_scale, device=dev)
+    pd.set_decode_removal(wl.decode_p)
     stream = torch.cuda.current_stream(dev)
     blocks = [(t0, min(wl.block, wl.s - t0)) for t0 in range(0, wl.s, wl.block)]
 
@@ -228,11 +241,10 @@ def gpu_bench(name, overrides, steps, warmup):
     es = 4 if wl.dtype == "f32" else 2
     flops = bmx.prefill_flops(b=wl.b, n_kv_heads=wl.n_kv_heads, group=G, head_dim=wl.head_dim,
                               s=wl.s, kv_max=wl.kv_max, block=wl.block)
-    dbytes = bmx.decode_bytes_per_step(b=wl.b, n_kv_heads=wl.n_kv_heads, group=G,
-                                       head_dim=wl.head_dim, kv_max=wl.kv_max, elem_bytes=es)
+    dbytes = decode_bytes(bmx, wl, wl.b)
     peak_f = PEAK_F32_MFMA if wl.dtype == "f32" else PEAK_BF16_MFMA
     prefill_tflops = flops / (pf_ms * 1e-3) / 1e12
-    decode_gbs = dbytes * wl.n_decode / (dec_ms * 1e-3) / 1e9 if wl.n_decode else 0.0
+    decode_gbs = dbytes / (dec_ms * 1e-3) / 1e9 if wl.n_decode else 0.0
     kernels = {
         "prefill_attention": {"bound": "mfma", "achieved": prefill_tflops,
                               "peak": peak_f / 1e12, "unit": "TFLOP/s",
@@ -243,7 +255,7 @@ def gpu_bench(name, overrides, steps, warmup):
         "decode_step": {"bound": "hbm", "achieved": decode_gbs, "peak": PEAK_HBM / 1e9,
                         "unit": "GB/s", "frac": decode_gbs / (PEAK_HBM / 1e9),
                         "ms_per_step": dec_ms, "launches_per_step": wl.n_decode,
-                        "algorithmic_per_launch": dbytes},
+                        "algorithmic_per_launch": dbytes / max(wl.n_decode, 1)},
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd = kernels[dom]
@@ -298,6 +310,8 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
     stack = bmx.PDStack(n_layers=wl.n_layers, b=b, s=wl.s, kv_max=wl.kv_max, block=wl.block,
                         max_gen=wl.n_decode, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads,
                         head_dim=wl.head_dim, dtype=wl.dtype, sm_scale=wl.sm_scale, device=dev)
+    for pd_ in stack.layers:
+        pd_.set_decode_removal(wl.decode_p)
     tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
     H, Hk, d, B = wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.block
     q = torch.empty((b, H, B, d), dtype=tdt, device=dev)
@@ -366,11 +380,10 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
     G = wl.group
     flops = L * bmx.prefill_flops(b=b, n_kv_heads=Hk, group=G, head_dim=d, s=wl.s,
                                   kv_max=wl.kv_max, block=B)
-    dbytes = L * bmx.decode_bytes_per_step(b=b, n_kv_heads=Hk, group=G, head_dim=d,
-                                           kv_max=wl.kv_max, elem_bytes=es)
+    dbytes = L * decode_bytes(bmx, wl, b)
     peak_f = PEAK_F32_MFMA if wl.dtype == "f32" else PEAK_BF16_MFMA
     prefill_tflops = flops / (pf_ms * 1e-3) / 1e12
-    decode_gbs = dbytes * wl.n_decode / (dec_ms * 1e-3) / 1e9
+    decode_gbs = dbytes / (dec_ms * 1e-3) / 1e9
     n_pf = L * len(blocks)
     kernels = {
         "prefill_attention": {"bound": "mfma", "achieved": prefill_tflops,
@@ -382,7 +395,7 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
         "decode_step": {"bound": "hbm", "achieved": decode_gbs, "peak": PEAK_HBM / 1e9,
                         "unit": "GB/s", "frac": decode_gbs / (PEAK_HBM / 1e9),
                         "ms_per_step": dec_ms, "launches_per_step": L * wl.n_decode,
-                        "algorithmic_per_launch": dbytes / L},
+                        "algorithmic_per_launch": dbytes / (L * max(wl.n_decode, 1))},
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd_ = kernels[dom]
@@ -425,6 +438,9 @@ def main():
                     help="layer stack only: run this batch instead of the largest that fits")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-p", type=int, default=0,
+                    help="decode removal schedule: 0 = one removal per step (default); p > 0 = "
+                         "Algorithm 1's decoding loop, p removals when a step starts full")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -442,7 +458,7 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    overrides = {}
+    overrides = {"decode_p": args.decode_p} if args.decode_p else {}
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, overrides, args.cpu_seconds)
@@ -468,6 +484,8 @@ def main():
         "config": {"workload": wl.name, "b": wl.b, "n_heads": wl.n_heads,
                    "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim, "s": wl.s,
                    "kv_max": wl.kv_max, "block": wl.block, "decode_steps": wl.n_decode,
+                   "decode_removal": (f"{wl.decode_p} at once when full" if wl.decode_p
+                                      else "one per step"),
                    "parallelism": "single GPU"},
         "roofline": res["roofline"],
         "cpu_baseline": cpu_baseline_line(cpu, wl) if cpu else None,

@@ -161,6 +161,19 @@ int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream);
 int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void* k, const void* v,
                    void* o, int32_t seq_ld, hipStream_t stream);
 
+/* Choose the decode removal schedule (default p = 0).
+ *   p = 0: each decode step appends its pair and, if the cache then holds more
+ *          than kv_max entries, removes the one with the smallest (ave, pos)
+ *          with curr_id = the step's position (one removal per step; the new
+ *          entry itself can be the one removed).
+ *   1 <= p <= kv_max: Algorithm 1's decoding loop taken literally -- when a
+ *          step starts with a full cache (kv_max entries), p entries are
+ *          removed first, ranked with curr_id = the last processed position;
+ *          the step then appends without removal, so the cache stays within
+ *          [kv_max - p, kv_max].
+ * BM_ERR_INVALID_ARG for p outside [0, kv_max]. */
+int bm_set_decode_removal(bm_ctx* ctx, int32_t p);
+
 /* Host copies of the uniform cache length and of the next expected position
  * (-1 for a null context). */
 int32_t bm_ctx_len(const bm_ctx* ctx);

@@ -77,6 +77,7 @@ def _load() -> ctypes.CDLL:
         "bm_resume": (ctypes.c_int, [dims_p, cache_p, I32, I32, ctypes.POINTER(P)]),
         "bm_prefill_block": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
         "bm_evict_compact": (ctypes.c_int, [P, I32, P]),
+        "bm_set_decode_removal": (ctypes.c_int, [P, I32]),
         "bm_decode_step": (ctypes.c_int, [P, I32, P, P, P, P, I32, P]),
         "bm_ctx_len": (I32, [P]),
         "bm_ctx_next_pos": (I32, [P]),
@@ -94,6 +95,7 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
             "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block", "bm_evict_compact",
+            "bm_set_decode_removal",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
             "bm_philox4x32_10")
 
@@ -146,6 +148,10 @@ def bm_prefill_block(ctx: int, t0: int, n_tok: int, q: int, k: int, v: int, o: i
 
 def bm_evict_compact(ctx: int, curr_id: int, stream: int) -> None:
     _check(_lib.bm_evict_compact(ctx, curr_id, stream))
+
+
+def bm_set_decode_removal(ctx: int, p: int) -> None:
+    _check(_lib.bm_set_decode_removal(ctx, p))
 
 
 def bm_decode_step(ctx: int, pos: int, q: int, k: int, v: int, o: int, seq_ld: int,
@@ -281,6 +287,11 @@ class PDAttention:
 
     def evict_compact(self, curr_id) -> None:
         bm_evict_compact(self.ctx, curr_id, self._stream())
+
+    def set_decode_removal(self, p: int) -> None:
+        """0: one removal per decode step after appending (default); p > 0:
+        Algorithm 1's decoding loop, p removals when a step starts full."""
+        bm_set_decode_removal(self.ctx, p)
 
     def decode_step(self, pos, q, k, v, o, row=0) -> None:
         H, Hk = self.dims.n_heads, self.dims.n_kv_heads
@@ -480,6 +491,21 @@ def prefill_flops(*, b, n_kv_heads, group, head_dim, s, kv_max, block) -> int:
         total += n * length + n * (n + 1) // 2
         length = min(kv_max, length + n)
     return 4 * head_dim * group * total * b * n_kv_heads
+
+
+def decode_cache_lengths(*, s, kv_max, n_decode, p=0) -> list:
+    """Cached entries each decode step's attention reads (before its own pair),
+    under the removal schedule chosen with ``bm_set_decode_removal``: the prompt
+    leaves min(s, kv_max); with p = 0 a step appends then removes one when over
+    the bound; with p > 0 a step that starts full first drops to kv_max - p."""
+    n = min(s, kv_max)
+    out = []
+    for _ in range(n_decode):
+        if p > 0 and n == kv_max:
+            n = kv_max - p
+        out.append(n)
+        n = min(n + 1, kv_max)
+    return out
 
 
 def decode_bytes_per_step(*, b, n_kv_heads, group, head_dim, kv_max, elem_bytes) -> int:

@@ -24,6 +24,7 @@ struct bm_ctx {
   int32_t len;        // live entries per unit (the same for every unit)
   int32_t next_pos;   // next position the schedule expects
   int32_t last_pos;   // last processed position, -1 before the first
+  int32_t p_dec;      // decode removal: 0 one per step after appending, p > 0 p at once when full
 };
 
 namespace {
@@ -160,6 +161,7 @@ int make_ctx(const bm_dims* dims, const bm_cache* cache, bm_ctx** out) {
   c->len = 0;
   c->next_pos = 0;
   c->last_pos = -1;
+  c->p_dec = 0;
   *out = c;
   return BM_OK;
 }
@@ -257,12 +259,11 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   return ok();
 }
 
-BM_EXPORT int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream) {
-  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
-  if (curr_id != ctx->last_pos)
-    return fail(BM_ERR_ORDER, "curr_id=%d but the last processed position is %d", curr_id,
-                ctx->last_pos);
-  if (ctx->len <= ctx->dims.kv_max) return ok();
+namespace {
+
+// Enqueue the cut of every unit from ctx->len down to `target` entries (select
+// + compaction), ranked at curr_id.  Requires ctx->len > target.
+int cut_to(bm_ctx* ctx, int target, int32_t curr_id, hipStream_t stream) {
   bm::EvictArgs a;
   a.kc = ctx->cache.k;
   a.vc = ctx->cache.v;
@@ -274,18 +275,41 @@ BM_EXPORT int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream)
   a.mcount = reinterpret_cast<int32_t*>(work_at(ctx, ctx->lay.mcount_off));
   a.cap = ctx->cap;
   a.n = ctx->len;
-  a.kv_max = ctx->dims.kv_max;
+  a.kv_max = target;
   a.curr_id = curr_id;
   a.units = ctx->units;
   a.head_dim = ctx->dims.head_dim;
   a.elem_bytes = ctx->elem_bytes;
   hipError_t e = bm::launch_select(a, stream);
   if (e != hipSuccess) return hip_fail(e, "select launch");
-  const int n_evict = ctx->len - ctx->dims.kv_max;
-  const int max_moves = n_evict < ctx->dims.kv_max ? n_evict : ctx->dims.kv_max;
-  e = bm::launch_compact(a, max_moves, stream);
-  if (e != hipSuccess) return hip_fail(e, "compact launch");
-  ctx->len = ctx->dims.kv_max;
+  const int n_evict = ctx->len - target;
+  const int max_moves = n_evict < target ? n_evict : target;
+  if (max_moves > 0) {
+    e = bm::launch_compact(a, max_moves, stream);
+    if (e != hipSuccess) return hip_fail(e, "compact launch");
+  }
+  ctx->len = target;
+  return BM_OK;
+}
+
+}  // namespace
+
+BM_EXPORT int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (curr_id != ctx->last_pos)
+    return fail(BM_ERR_ORDER, "curr_id=%d but the last processed position is %d", curr_id,
+                ctx->last_pos);
+  if (ctx->len <= ctx->dims.kv_max) return ok();
+  const int st = cut_to(ctx, ctx->dims.kv_max, curr_id, stream);
+  return st == BM_OK ? ok() : st;
+}
+
+BM_EXPORT int bm_set_decode_removal(bm_ctx* ctx, int32_t p) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (p < 0 || p > ctx->dims.kv_max)
+    return fail(BM_ERR_INVALID_ARG, "decode removal p=%d outside [0, kv_max=%d]", p,
+                ctx->dims.kv_max);
+  ctx->p_dec = p;
   return ok();
 }
 
@@ -307,6 +331,12 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
   if (ctx->len > ctx->dims.kv_max)
     return fail(BM_ERR_CAPACITY, "cache holds %d > kv_max=%d entries: evict after the last block",
                 ctx->len, ctx->dims.kv_max);
+  // Algorithm 1's decoding loop taken literally: a full cache first loses p_dec
+  // entries, ranked at the last processed position; the step then only appends
+  if (ctx->p_dec > 0 && ctx->len == ctx->dims.kv_max) {
+    const int st = cut_to(ctx, ctx->dims.kv_max - ctx->p_dec, ctx->last_pos, stream);
+    if (st != BM_OK) return st;
+  }
   bm::DecodeArgs a;
   a.q = q;
   a.kin = k;

@@ -65,6 +65,7 @@ class Workload:
     span_len: int = 64
     n_layers: int = 1
     seed: int = 1
+    decode_p: int = 0     # 0: one removal per decode step; p > 0: Algorithm 1's p at once
 
     @property
     def group(self) -> int:

@@ -114,14 +114,20 @@ def _compare_cut(tag, orc: opd.StepOracle, ev, gpu_pos, st: Stats):
 
 
 def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decode_steps=None,
-               inputs=None, pd=None, stop_on_failure=True) -> Stats:
-    """Run the whole P&D schedule on the device and compare the checked units."""
+               inputs=None, pd=None, stop_on_failure=True, decode_p=0) -> Stats:
+    """Run the whole P&D schedule on the device and compare the checked units.
+
+    ``decode_p > 0`` selects Algorithm 1's decoding loop taken literally (a step
+    that starts with a full cache first removes ``decode_p`` entries); the cut
+    is compared against the device's live set without the step's new entry."""
     st = Stats()
     if inputs is None:
         inputs = synth.batch_inputs(wl, device, checked=checked, sharp=sharp)
     q, k, v = inputs
     o = torch.zeros_like(q)
     pd = pd or make_pd(wl, device)
+    if decode_p:
+        pd.set_decode_removal(decode_p)
     G = wl.group
     uin = {u: synth.unit_inputs(wl, 0, u[0], u[1], sharp=sharp) for u in checked}
     orcs = {u: opd.StepOracle(head_dim=wl.head_dim, group=G, kv_max=wl.kv_max,
@@ -165,9 +171,20 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
         pos, score, dlen = _snapshot(pd, checked, length)
         for i, u in enumerate(checked):
             uq, uk, uv = uin[u]
-            ref, ev = orcs[u].decode_step(p, uq[:, p], uk[p], uv[p])
+            if decode_p:
+                # the oracle's step taken apart (the cut, then append + attend, as in
+                # UnitOracle.decode_step_alg1) so a near-tie cut can be adopted before
+                # the new entry is attended
+                orc = orcs[u]
+                if orc.n == wl.kv_max:
+                    ev = orc.evict(p - 1, "decode", target=wl.kv_max - decode_p)
+                    _compare_cut(f"decode {p} unit {u}", orc, ev, pos[i][pos[i] != p], st)
+                orc.append(p, uk[p][None], uv[p][None])
+                ref = orc.attend(uq[:, p][:, None, :], p)[:, 0, :]
+            else:
+                ref, ev = orcs[u].decode_step(p, uq[:, p], uk[p], uv[p])
+                _compare_cut(f"decode {p} unit {u}", orcs[u], ev, pos[i], st)
             check_out(f"decode {p}", u, slice(p, p + 1), ref[:, None, :])
-            _compare_cut(f"decode {p} unit {u}", orcs[u], ev, pos[i], st)
             _compare_state(f"decode {p} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st)
         if stop_on_failure and st.failures:
             return st

@@ -179,6 +179,20 @@ def test_decode_order_and_capacity_errors():
         bmx.bm_destroy(ctx)
 
 
+def test_decode_removal_range():
+    d = dims()
+    ctx = _ctx(d, 128, 520)
+    try:
+        for p in (0, 1, d.kv_max):
+            bmx.bm_set_decode_removal(ctx, p)
+        assert status_of(bmx.bm_set_decode_removal, ctx, -1) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_set_decode_removal, ctx, d.kv_max + 1) == bmx.BM_ERR_INVALID_ARG
+        assert bmx.bm_ctx_len(ctx) == 128            # choosing the schedule does no work
+    finally:
+        bmx.bm_destroy(ctx)
+    assert status_of(bmx.bm_set_decode_removal, None, 1) == bmx.BM_ERR_INVALID_ARG
+
+
 def test_null_context():
     P = FAKE
     assert status_of(bmx.bm_prefill_block, None, 0, 1, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
@@ -213,3 +227,36 @@ def test_synth_argument_checks():
     assert call(mk(b=0), 0, 4, FAKE, FAKE, FAKE, 4) == bad
     assert status_of(bmx.bm_philox4x32_10, FAKE, FAKE, 0, 0) == bad
     assert status_of(bmx.bm_philox4x32_10, 0, FAKE, 4, 0) == bad
+
+
+@pytest.mark.parametrize("p", [0, 1, 3, 8])
+def test_decode_cache_lengths_follow_the_oracle(p):
+    # the host's schedule model (used for the decode roofline) against the
+    # oracle stepping the same schedule: entries each step's attention reads
+    import numpy as np
+
+    from oracle import pd as opd
+
+    s, kv_max, block, n_decode, d = 20, 8, 4, 15, 4
+    rng = np.random.default_rng(3)
+    unit = opd.UnitOracle(head_dim=d, group=1, kv_max=kv_max, sm_scale=0.5)
+    for t0 in range(0, s, block):
+        unit.prefill_block(t0, rng.standard_normal((1, block, d)),
+                           rng.standard_normal((block, d)), rng.standard_normal((block, d)))
+        unit.evict(t0 + block - 1, "prefill")
+    seen = []
+    for t in range(n_decode):
+        pos = s + t
+        q, k, v = rng.standard_normal((1, d)), rng.standard_normal(d), rng.standard_normal(d)
+        if p:
+            if unit.n == kv_max:
+                unit.evict(pos - 1, "decode", target=kv_max - p)
+            seen.append(unit.n)
+            unit.append(pos, k[None], v[None])
+            unit.attend(q[:, None, :], pos)
+        else:
+            seen.append(unit.n)
+            unit.decode_step(pos, q, k, v)
+    assert bmx.decode_cache_lengths(s=s, kv_max=kv_max, n_decode=n_decode, p=p) == seen
+    # prompt shorter than the bound: the cache first fills during decode
+    assert bmx.decode_cache_lengths(s=5, kv_max=8, n_decode=6, p=2) == [5, 6, 7, 6, 7, 6]

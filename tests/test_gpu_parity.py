@@ -91,6 +91,23 @@ def test_bound_larger_than_prompt_then_decode_cuts():
     assert st.cuts == wl.units * (300 + 20 - 310)
 
 
+@pytest.mark.parametrize("p", [1, 8, 512])
+def test_alg1_decode_removal_c2_shape(p):
+    # Algorithm 1's decoding loop taken literally: p removals whenever a step
+    # starts with a full cache (p = kv_max empties it); the prompt leaves it full
+    wl = C2.with_(b=2, s=1024, n_decode=24)
+    st = _run(wl, synth.checked_units(wl, wl.units), decode_p=p)
+    assert st.cuts == wl.units * (1024 // 256 - 512 // 256 + -(-24 // p))
+
+
+def test_alg1_decode_removal_ragged_fp32_bound_above_prompt():
+    # cache first fills during decode (step kv_max - s), then p = 4 at a time
+    wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, dtype="f32", b=2, n_heads=8,
+                  n_kv_heads=2, head_dim=64, s=300, kv_max=310, block=48, n_decode=20)
+    st = _run(wl, synth.checked_units(wl, wl.units), decode_p=4)
+    assert st.cuts == wl.units * 3
+
+
 def test_sharp_distribution():
     wl = C2.with_(b=2, s=2048, n_decode=32)
     st = _run(wl, synth.checked_units(wl, wl.units), sharp=True)

@@ -59,6 +59,7 @@ class UnitOracle:
     group: int          # G query heads per KV head
     kv_max: int         # the paper's maximum cache size |kv|-bar
     sm_scale: float
+    rule: str = "ave"   # ranking key of a cut, see ``ranking_key``
     pos: np.ndarray = field(default=None)
     k: np.ndarray = field(default=None)
     v: np.ndarray = field(default=None)
@@ -128,20 +129,39 @@ class UnitOracle:
         """
         return self.score / (curr_id + 1 - self.pos).astype(np.float64)
 
+    def ranking_key(self, curr_id: int) -> np.ndarray:
+        """The key whose smallest entries a cut removes.
+
+        ``"ave"``: ``ave_weights`` (Sec. 3.2; the method).  ``"sum"``: the
+        accumulated ``sum_weights`` itself, the cumulative rule that Sec. 3.2
+        corrects because it favours early tokens.  ``"recent"``: the position,
+        so the most recent pairs stay (the eviction of Algorithm 3, the
+        extreme decoding-only comparator of Sec. 4).
+        """
+        if self.rule == "ave":
+            return self.averages(curr_id)
+        if self.rule == "sum":
+            return self.score.copy()
+        if self.rule == "recent":
+            return self.pos.astype(np.float64)
+        raise ValueError(f"unknown ranking rule {self.rule!r}")
+
     def evict(self, curr_id: int, kind: str, target: int | None = None) -> EvictionEvent | None:
         """Cut the cache back to ``target`` (default ``kv_max``) entries (Sec. 3.1;
         Sec. 3.2 rule).
 
-        The entries with the smallest ``ave_weights`` are removed; on an exact
-        tie the older entry (smaller position) goes first (reading R8).  No-op
-        while the cache holds at most ``target`` entries (reading R16).
-        Survivors keep their accumulated scores (reading R13).
+        The entries with the smallest ranking key (``ave_weights`` under the
+        paper's rule) are removed; on an exact tie the older entry (smaller
+        position) goes first (reading R8).  No-op while the cache holds at most
+        ``target`` entries (reading R16).  Survivors keep their accumulated
+        scores (reading R13).  ``all_ave`` and ``gap`` of the event are in the
+        rule's key.
         """
         target = self.kv_max if target is None else target
         n = self.n
         if n <= target:
             return None
-        ave = self.averages(curr_id)
+        ave = self.ranking_key(curr_id)
         order = np.lexsort((self.pos, ave))        # ascending ave, then ascending pos
         n_evict = n - target
         evict_idx = order[:n_evict]
@@ -174,26 +194,32 @@ class UnitOracle:
         self.append(t0, k, v)
         return self.attend(q, t0)
 
-    def decode_step(self, pos: int, q: np.ndarray, k: np.ndarray, v: np.ndarray):
+    def decode_step(self, pos: int, q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                    bound: int | None = None):
         """One decode step at position ``pos`` with one eviction (reading R3).
 
         Algorithm 1 decode loop (Sec. 3.1) with one KV pair removed per step:
-        append, attend with ``curr_id = pos``, then cut back to ``kv_max``.
-        ``q`` is ``[G, d]``; returns (outputs ``[G, d]``, event or None).
+        append, attend with ``curr_id = pos``, then cut back to ``bound``
+        (default ``kv_max``).  ``q`` is ``[G, d]``; returns (outputs ``[G, d]``,
+        event or None).
         """
         self.append(pos, np.asarray(k)[None], np.asarray(v)[None])
         o = self.attend(np.asarray(q)[:, None, :], pos)[:, 0, :]
-        return o, self.evict(pos, "decode")
+        return o, self.evict(pos, "decode", target=bound)
 
-    def decode_step_alg1(self, pos: int, q: np.ndarray, k: np.ndarray, v: np.ndarray, p: int):
+    def decode_step_alg1(self, pos: int, q: np.ndarray, k: np.ndarray, v: np.ndarray, p: int,
+                         bound: int | None = None):
         """One decode step of Algorithm 1's decoding loop taken literally: when
-        the cache holds ``kv_max`` entries, first remove ``p`` of them (ranked
-        with ``curr_id = pos - 1``, the last processed position, reading R4),
-        then process the token at ``pos`` (append and attend, no removal).
+        the cache holds ``bound`` (default ``kv_max``) entries or more, first
+        cut it to ``bound - p`` (ranked with ``curr_id = pos - 1``, the last
+        processed position, reading R4), then process the token at ``pos``
+        (append and attend, no removal).  Algorithm 3's decoding loop is the
+        case ``bound = 2``, ``p = 1`` under the ``"recent"`` rule.
         Returns (outputs ``[G, d]``, event or None)."""
+        bound = self.kv_max if bound is None else bound
         ev = None
-        if self.n == self.kv_max:
-            ev = self.evict(pos - 1, "decode", target=self.kv_max - p)
+        if self.n >= bound:
+            ev = self.evict(pos - 1, "decode", target=bound - p)
         self.append(pos, np.asarray(k)[None], np.asarray(v)[None])
         o = self.attend(np.asarray(q)[:, None, :], pos)[:, 0, :]
         return o, ev
@@ -244,7 +270,8 @@ class Trace:
 
 
 def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
-             sm_scale: float, p_dec: int = 0) -> Trace:
+             sm_scale: float, p_dec: int = 0, rule: str = "ave",
+             kv_dec: int | None = None) -> Trace:
     """Full P&D run of one unit (Sec. 3.1, Algorithm 1 under reading R1).
 
     ``q`` is ``[G, s + n_decode, d]``; ``k``, ``v`` are ``[s + n_decode, d]``,
@@ -255,12 +282,20 @@ def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
     and cuts with curr_id = s + t; with ``p_dec > 0`` it follows Algorithm 1's
     decoding loop literally instead (``decode_step_alg1``: remove ``p_dec``
     entries when the cache is full, before the token is processed).
+
+    ``rule`` picks the ranking key (``UnitOracle.ranking_key``).  ``kv_dec``
+    bounds the cache during decode (default ``kv_max``); with ``p_dec = 0`` a
+    cache larger than ``kv_dec`` at the first step is first cut to ``kv_dec``
+    with curr_id = the last processed position.  Algorithm 3 (ED): ``kv_max >=
+    s`` (no removal while prefilling), ``kv_dec = 2``, ``p_dec = 1``,
+    ``rule = "recent"``.
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     g_heads, total, d = q.shape
-    unit = UnitOracle(head_dim=d, group=g_heads, kv_max=kv_max, sm_scale=sm_scale)
+    unit = UnitOracle(head_dim=d, group=g_heads, kv_max=kv_max, sm_scale=sm_scale, rule=rule)
+    kd = kv_max if kv_dec is None else kv_dec
     out = np.zeros((g_heads, total, d))
     events = []
     t0 = 0
@@ -274,9 +309,11 @@ def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
     for t in range(n_decode):
         i = s + t
         if p_dec > 0:
-            out[:, i], ev = unit.decode_step_alg1(i, q[:, i], k[i], v[i], p_dec)
+            out[:, i], ev = unit.decode_step_alg1(i, q[:, i], k[i], v[i], p_dec, bound=kd)
         else:
-            out[:, i], ev = unit.decode_step(i, q[:, i], k[i], v[i])
+            if unit.n > kd:
+                events.append(unit.evict(i - 1, "decode", target=kd))
+            out[:, i], ev = unit.decode_step(i, q[:, i], k[i], v[i], bound=kd)
         if ev is not None:
             events.append(ev)
     order = np.argsort(unit.pos)

@@ -289,9 +289,74 @@ def pin_super_key(cls):
     assert sc > 0.99 * n_after
 
 
+def pin_rule_keys_bruteforce(cls):
+    """Under every ranking rule the kept set is the unique subset whose every
+    member ranks above every removed entry under (key, pos), with the key
+    written from its definition: ave_weights (Sec. 3.2), the accumulated
+    sum_weights (the cumulative rule Sec. 3.2 corrects), the position
+    (Algorithm 3 keeps the most recent pairs).  Includes a hand-made case where
+    the three rules disagree."""
+    curr_id = 10
+    # pos 0 with sum 3 (ave 3/11), pos 9 with sum 1 (ave 1/2), pos 5 with sum 2 (ave 1/3)
+    want = {"ave": [9], "sum": [0], "recent": [9]}
+    for rule, kept in want.items():
+        u = cls(head_dim=2, group=1, kv_max=1, sm_scale=1.0, rule=rule)
+        u.pos, u.score = np.array([0, 9, 5], dtype=np.int64), np.array([3.0, 1.0, 2.0])
+        u.k, u.v = np.zeros((3, 2)), np.zeros((3, 2))
+        ev = u.evict(curr_id, "prefill")
+        assert list(ev.kept_pos) == kept, rule
+    rng = np.random.default_rng(37)
+    for trial in range(60):
+        rule = ("ave", "sum", "recent")[trial % 3]
+        n = int(rng.integers(3, 10))
+        kv_max = int(rng.integers(1, n))
+        pos = rng.choice(np.arange(0, curr_id + 30), size=n, replace=False)
+        score = rng.integers(0, 3, size=n).astype(np.float64) / 2.0   # frequent exact ties
+        u = cls(head_dim=2, group=1, kv_max=kv_max, sm_scale=1.0, rule=rule)
+        u.pos, u.score = pos.astype(np.int64), score
+        u.k, u.v = np.zeros((n, 2)), np.zeros((n, 2))
+        c = int(pos.max())
+        ev = u.evict(c, "prefill")
+        key = {"ave": lambda sc, p: sc / (c + 1 - p), "sum": lambda sc, p: sc,
+               "recent": lambda sc, p: float(p)}[rule]
+        rank = {int(p): (key(sc, int(p)), int(p)) for p, sc in zip(pos, score)}
+        valid = [list(kept) for kept in itertools.combinations(sorted(rank), kv_max)
+                 if min(rank[p] for p in kept) > max(rank[p] for p in set(rank) - set(kept))]
+        assert len(valid) == 1 and list(ev.kept_pos) == valid[0], rule
+
+
+def pin_alg3_closed_form(cls):
+    """Algorithm 3 (ED): no removal while prefilling (bound >= s), then every
+    decode step attends over exactly the previous token and itself, so each
+    output is the two-term softmax average written out by hand; prefill outputs
+    are dense causal attention (SDPA); the cache ends with the last two
+    positions."""
+    rng = np.random.default_rng(41)
+    G, s, D, d = 2, 12, 6, 8
+    q, k, v = _rand_unit(rng, G, s + D, d)
+    sm = 0.7
+    u = cls(head_dim=d, group=G, kv_max=s, sm_scale=sm, rule="recent")
+    out = np.zeros((G, s + D, d))
+    out[:, :s] = u.prefill_block(0, q[:, :s], k[:s], v[:s])
+    for t in range(D):
+        i = s + t
+        out[:, i], _ = u.decode_step_alg1(i, q[:, i], k[i], v[i], 1, bound=2)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.tensor(q[:, :s]), torch.tensor(k[:s])[None].expand(G, s, d),
+        torch.tensor(v[:s])[None].expand(G, s, d), is_causal=True, scale=sm).numpy()
+    np.testing.assert_allclose(out[:, :s], ref, rtol=0, atol=1e-12)
+    for t in range(D):
+        i = s + t
+        for g in range(G):
+            z0, z1 = sm * q[g, i] @ k[i - 1], sm * q[g, i] @ k[i]
+            w0, w1 = 1.0 / (1.0 + np.exp(z1 - z0)), 1.0 / (1.0 + np.exp(z0 - z1))
+            np.testing.assert_allclose(out[g, i], w0 * v[i - 1] + w1 * v[i], rtol=0, atol=1e-12)
+    assert sorted(int(p) for p in u.pos) == [s + D - 2, s + D - 1]
+
+
 ALL_PINS = [pin_dense_fixed_point, pin_golden, pin_selection_bruteforce,
             pin_conservation_and_lengths, pin_paper_stated_values, pin_permutation_invariance,
-            pin_micro_agreement, pin_super_key]
+            pin_micro_agreement, pin_super_key, pin_rule_keys_bruteforce, pin_alg3_closed_form]
 
 
 @pytest.mark.parametrize("pin", ALL_PINS, ids=lambda f: f.__name__)
@@ -371,13 +436,14 @@ class _NoSelfAttention(opd.StepOracle):
 
 
 class _TieNewestFirst(opd.StepOracle):
-    def evict(self, curr_id, kind):
+    def evict(self, curr_id, kind, target=None):
+        target = self.kv_max if target is None else target
         n = self.n
-        if n <= self.kv_max:
+        if n <= target:
             return None
-        ave = self.averages(curr_id)
+        ave = self.ranking_key(curr_id)
         order = np.lexsort((-self.pos, ave))
-        n_evict = n - self.kv_max
+        n_evict = n - target
         keep = np.sort(order[n_evict:])
         by = np.argsort(self.pos)
         ev = opd.EvictionEvent(kind, curr_id, n, np.sort(self.pos[keep]),
@@ -423,8 +489,23 @@ class _EvictLargest(opd.StepOracle):
         return -super().averages(curr_id)
 
 
+class _SumRuleUsesAverages(opd.StepOracle):
+    def ranking_key(self, curr_id):
+        if self.rule == "sum":
+            return self.averages(curr_id)
+        return super().ranking_key(curr_id)
+
+
+class _RecentKeepsOldest(opd.StepOracle):
+    def ranking_key(self, curr_id):
+        if self.rule == "recent":
+            return -self.pos.astype(np.float64)
+        return super().ranking_key(curr_id)
+
+
 @pytest.mark.parametrize("mutant", [_DenomOffByOne, _NoSelfAttention, _TieNewestFirst,
-                                    _FirstHeadOnly, _NoScale, _TransposedValues, _EvictLargest],
+                                    _FirstHeadOnly, _NoScale, _TransposedValues, _EvictLargest,
+                                    _SumRuleUsesAverages, _RecentKeepsOldest],
                          ids=lambda c: c.__name__)
 def test_planted_mistake_is_caught(mutant):
     failures = 0
@@ -497,3 +578,40 @@ def test_alg1_decode_matches_dense_when_bound_is_never_reached():
     a = opd.run_unit(q, k, v, s=s, kv_max=64, block=4, n_decode=D, sm_scale=0.25)
     b = opd.run_unit(q, k, v, s=s, kv_max=64, block=4, n_decode=D, sm_scale=0.25, p_dec=5)
     assert np.array_equal(a.out, b.out) and not b.events
+
+
+def test_run_unit_ed_mode_is_algorithm_3():
+    """run_unit's ED configuration (no prefill removal, decode bound 2, p = 1,
+    most-recent rule) reproduces Algorithm 3 stepped by hand, and its decode
+    outputs only ever see two entries."""
+    rng = np.random.default_rng(43)
+    G, s, D, d = 2, 10, 5, 4
+    q, k, v = _rand_unit(rng, G, s + D, d)
+    tr = opd.run_unit(q, k, v, s=s, kv_max=s, block=4, n_decode=D, sm_scale=0.5, p_dec=1,
+                      rule="recent", kv_dec=2)
+    u = opd.UnitOracle(head_dim=d, group=G, kv_max=s, sm_scale=0.5, rule="recent")
+    u.prefill_block(0, q[:, :s], k[:s], v[:s])
+    keep = u.evict(s - 1, "decode", target=1)          # remove all but the most recent
+    assert list(keep.kept_pos) == [s - 1]
+    for t in range(D):
+        i = s + t
+        u.append(i, k[i:i + 1], v[i:i + 1])
+        assert u.n == 2
+        o = u.attend(q[:, i:i + 1], i)[:, 0]
+        np.testing.assert_allclose(tr.out[:, i], o, rtol=0, atol=1e-13)
+        u.evict(i, "decode", target=1)
+    assert len(tr.events) == D
+
+
+def test_run_unit_decode_bound_with_one_removal_per_step():
+    """p = 0 with a decode bound below the prefill bound: the first step cuts
+    to the decode bound at the last processed position, then one removal per
+    step keeps the bound."""
+    rng = np.random.default_rng(47)
+    G, s, D, d = 1, 16, 6, 4
+    q, k, v = _rand_unit(rng, G, s + D, d)
+    tr = opd.run_unit(q, k, v, s=s, kv_max=12, block=4, n_decode=D, sm_scale=0.5, kv_dec=5)
+    dec = [e for e in tr.events if e.kind == "decode"]
+    assert dec[0].curr_id == s - 1 and len(dec[0].kept_pos) == 5
+    assert all(len(e.kept_pos) == 5 for e in dec[1:]) and len(dec) == D + 1
+    assert len(tr.final_pos) == 5

@@ -59,11 +59,22 @@ typedef enum bm_status {
 
 typedef enum bm_dtype { BM_F32 = 0, BM_BF16 = 1 } bm_dtype;
 
+/* What a cut ranks by (bm_set_rank_rule); every rule removes the smallest
+ * keys first and, on an exact tie, the older entry. */
+typedef enum bm_rank_rule {
+  BM_RANK_AVE = 0,    /* score / (curr_id + 1 - pos): the method (Sec. 3.2)        */
+  BM_RANK_SUM = 1,    /* score alone: the cumulative rule Sec. 3.2 corrects        */
+  BM_RANK_RECENT = 2  /* pos: keep the most recent pairs (Algorithm 3, the
+                         extreme decoding-only comparator of Sec. 4)               */
+} bm_rank_rule;
+
 /* Problem statement (Sec. 3 and Algorithm 1): batch b, padded prompt length
  * s (s-bar), cache bound kv_max (|kv|-bar), prefill block (the removal amount
  * p of Algorithm 1), decode steps max_gen, and the attention shape.
  * Supported: head_dim 64 or 128; group n_heads / n_kv_heads of 1, 2 or 4;
- * 1 <= block <= 1024; kv_max >= 1; kv_max + block <= 4096. */
+ * 1 <= block <= 1024; kv_max >= 1; kv_max + block <= 65536.  A cut of more
+ * than 4096 live entries streams its keys from memory (slower); one decode
+ * step attends to at most 4097 entries (BM_ERR_UNSUPPORTED beyond). */
 typedef struct bm_dims {
   int32_t b;
   int32_t s;
@@ -173,6 +184,29 @@ int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void* k, const
  *          [kv_max - p, kv_max].
  * BM_ERR_INVALID_ARG for p outside [0, kv_max]. */
 int bm_set_decode_removal(bm_ctx* ctx, int32_t p);
+
+/* Choose the ranking key of every later cut (default BM_RANK_AVE), in
+ * bm_evict_compact and in decode steps.  BM_ERR_INVALID_ARG for an unknown
+ * rule. */
+int bm_set_rank_rule(bm_ctx* ctx, int32_t rule);
+
+/* Cache bound during decode (default kv_max; 1 <= bound <= kv_max, else
+ * BM_ERR_INVALID_ARG).  Decode steps then use `bound` where the schedule
+ * above says kv_max; a cache larger than `bound` at a decode step is first
+ * cut to `bound` (p = 0) or to bound - p (p > 0), ranked with curr_id = the
+ * last processed position.  Algorithm 3 (extreme decoding-only, Sec. 4):
+ * kv_max >= s (nothing removed while prefilling), bound 2, p = 1,
+ * BM_RANK_RECENT.  A decode step with p > bound returns BM_ERR_INVALID_ARG. */
+int bm_set_decode_bound(bm_ctx* ctx, int32_t bound);
+
+/* Score accumulation during prefill (default on = 1).  Off (0): later
+ * bm_prefill_block calls compute the attention outputs only (new entries get
+ * score 0), the prefill of the full-cache and decoding-only comparators of
+ * Sec. 4; decode steps still add their probabilities.  Once a block has run
+ * without accumulation, a cut ranked by BM_RANK_AVE or BM_RANK_SUM returns
+ * BM_ERR_ORDER (its scores would miss that block) until the context is
+ * rebuilt. */
+int bm_set_score_accumulation(bm_ctx* ctx, int32_t on);
 
 /* Host copies of the uniform cache length and of the next expected position
  * (-1 for a null context). */

@@ -23,6 +23,8 @@ LIB_PATH = os.path.join(HERE, "libbatchmax.so")
 
 BM_OK, BM_ERR_INVALID_ARG, BM_ERR_UNSUPPORTED, BM_ERR_CAPACITY, BM_ERR_ORDER, BM_ERR_HIP = range(6)
 BM_F32, BM_BF16 = 0, 1
+BM_RANK_AVE, BM_RANK_SUM, BM_RANK_RECENT = 0, 1, 2
+RANK_RULES = {"ave": BM_RANK_AVE, "sum": BM_RANK_SUM, "recent": BM_RANK_RECENT}
 STATUS_NAMES = {0: "BM_OK", 1: "BM_ERR_INVALID_ARG", 2: "BM_ERR_UNSUPPORTED",
                 3: "BM_ERR_CAPACITY", 4: "BM_ERR_ORDER", 5: "BM_ERR_HIP"}
 
@@ -78,6 +80,9 @@ def _load() -> ctypes.CDLL:
         "bm_prefill_block": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
         "bm_evict_compact": (ctypes.c_int, [P, I32, P]),
         "bm_set_decode_removal": (ctypes.c_int, [P, I32]),
+        "bm_set_rank_rule": (ctypes.c_int, [P, I32]),
+        "bm_set_decode_bound": (ctypes.c_int, [P, I32]),
+        "bm_set_score_accumulation": (ctypes.c_int, [P, I32]),
         "bm_decode_step": (ctypes.c_int, [P, I32, P, P, P, P, I32, P]),
         "bm_ctx_len": (I32, [P]),
         "bm_ctx_next_pos": (I32, [P]),
@@ -95,7 +100,8 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
             "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block", "bm_evict_compact",
-            "bm_set_decode_removal",
+            "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
+            "bm_set_score_accumulation",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
             "bm_philox4x32_10")
 
@@ -152,6 +158,18 @@ def bm_evict_compact(ctx: int, curr_id: int, stream: int) -> None:
 
 def bm_set_decode_removal(ctx: int, p: int) -> None:
     _check(_lib.bm_set_decode_removal(ctx, p))
+
+
+def bm_set_rank_rule(ctx: int, rule: int) -> None:
+    _check(_lib.bm_set_rank_rule(ctx, rule))
+
+
+def bm_set_decode_bound(ctx: int, bound: int) -> None:
+    _check(_lib.bm_set_decode_bound(ctx, bound))
+
+
+def bm_set_score_accumulation(ctx: int, on: int) -> None:
+    _check(_lib.bm_set_score_accumulation(ctx, on))
 
 
 def bm_decode_step(ctx: int, pos: int, q: int, k: int, v: int, o: int, seq_ld: int,
@@ -292,6 +310,16 @@ class PDAttention:
         """0: one removal per decode step after appending (default); p > 0:
         Algorithm 1's decoding loop, p removals when a step starts full."""
         bm_set_decode_removal(self.ctx, p)
+
+    def set_rank_rule(self, rule) -> None:
+        """"ave" (default, Sec. 3.2), "sum" or "recent" (or a BM_RANK_* value)."""
+        bm_set_rank_rule(self.ctx, RANK_RULES.get(rule, rule))
+
+    def set_decode_bound(self, bound: int) -> None:
+        bm_set_decode_bound(self.ctx, bound)
+
+    def set_score_accumulation(self, on: bool) -> None:
+        bm_set_score_accumulation(self.ctx, 1 if on else 0)
 
     def decode_step(self, pos, q, k, v, o, row=0) -> None:
         H, Hk = self.dims.n_heads, self.dims.n_kv_heads

@@ -25,6 +25,10 @@ struct bm_ctx {
   int32_t next_pos;   // next position the schedule expects
   int32_t last_pos;   // last processed position, -1 before the first
   int32_t p_dec;      // decode removal: 0 one per step after appending, p > 0 p at once when full
+  int32_t kv_dec;     // cache bound during decode (<= kv_max)
+  int32_t rule;       // bm_rank_rule of every cut
+  bool accumulate;    // prefill adds probabilities to the scores
+  bool scores_valid;  // no block has run without accumulation
 };
 
 namespace {
@@ -72,9 +76,9 @@ int check_dims(const bm_dims* d) {
     return fail(BM_ERR_UNSUPPORTED, "query heads per KV head %d unsupported (1, 2 or 4)", g);
   if (d->block > bm::kMaxBlock)
     return fail(BM_ERR_UNSUPPORTED, "block %d exceeds %d", d->block, bm::kMaxBlock);
-  if ((int64_t)d->kv_max + d->block > bm::kMaxCap)
+  if ((int64_t)d->kv_max + d->block > bm::kMaxCapAny)
     return fail(BM_ERR_UNSUPPORTED, "kv_max + block = %lld exceeds %d",
-                (long long)d->kv_max + d->block, bm::kMaxCap);
+                (long long)d->kv_max + d->block, bm::kMaxCapAny);
   if ((int64_t)d->b * d->n_kv_heads > (1 << 24))
     return fail(BM_ERR_UNSUPPORTED, "b * n_kv_heads too large");
   return BM_OK;
@@ -162,6 +166,10 @@ int make_ctx(const bm_dims* dims, const bm_cache* cache, bm_ctx** out) {
   c->next_pos = 0;
   c->last_pos = -1;
   c->p_dec = 0;
+  c->kv_dec = dims->kv_max;
+  c->rule = BM_RANK_AVE;
+  c->accumulate = true;
+  c->scores_valid = true;
   *out = c;
   return BM_OK;
 }
@@ -248,6 +256,7 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   a.npt_used = (n_tok + ppw - 1) / ppw;
   a.npt_stride = ctx->lay.npt;
   a.units = ctx->units;
+  a.accumulate = ctx->accumulate ? 1 : 0;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
   hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
@@ -256,13 +265,23 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   ctx->len += n_tok;
   ctx->next_pos = t0 + n_tok;
   ctx->last_pos = t0 + n_tok - 1;
+  if (!ctx->accumulate) ctx->scores_valid = false;
   return ok();
 }
 
 namespace {
 
+// A cut ranked by the scores needs every block's probabilities in them.
+int check_rule(const bm_ctx* ctx) {
+  if (!ctx->scores_valid && ctx->rule != BM_RANK_RECENT)
+    return fail(BM_ERR_ORDER,
+                "a block ran without score accumulation: only BM_RANK_RECENT can rank this cache");
+  return BM_OK;
+}
+
 // Enqueue the cut of every unit from ctx->len down to `target` entries (select
-// + compaction), ranked at curr_id.  Requires ctx->len > target.
+// + compaction), ranked at curr_id.  Requires ctx->len > target; the caller has
+// checked the rule.
 int cut_to(bm_ctx* ctx, int target, int32_t curr_id, hipStream_t stream) {
   bm::EvictArgs a;
   a.kc = ctx->cache.k;
@@ -280,6 +299,7 @@ int cut_to(bm_ctx* ctx, int target, int32_t curr_id, hipStream_t stream) {
   a.units = ctx->units;
   a.head_dim = ctx->dims.head_dim;
   a.elem_bytes = ctx->elem_bytes;
+  a.rule = ctx->rule;
   hipError_t e = bm::launch_select(a, stream);
   if (e != hipSuccess) return hip_fail(e, "select launch");
   const int n_evict = ctx->len - target;
@@ -300,8 +320,34 @@ BM_EXPORT int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream)
     return fail(BM_ERR_ORDER, "curr_id=%d but the last processed position is %d", curr_id,
                 ctx->last_pos);
   if (ctx->len <= ctx->dims.kv_max) return ok();
-  const int st = cut_to(ctx, ctx->dims.kv_max, curr_id, stream);
+  int st = check_rule(ctx);
+  if (st != BM_OK) return st;
+  st = cut_to(ctx, ctx->dims.kv_max, curr_id, stream);
   return st == BM_OK ? ok() : st;
+}
+
+BM_EXPORT int bm_set_rank_rule(bm_ctx* ctx, int32_t rule) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (rule != BM_RANK_AVE && rule != BM_RANK_SUM && rule != BM_RANK_RECENT)
+    return fail(BM_ERR_INVALID_ARG, "unknown ranking rule %d", rule);
+  ctx->rule = rule;
+  return ok();
+}
+
+BM_EXPORT int bm_set_decode_bound(bm_ctx* ctx, int32_t bound) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (bound < 1 || bound > ctx->dims.kv_max)
+    return fail(BM_ERR_INVALID_ARG, "decode bound %d outside [1, kv_max=%d]", bound,
+                ctx->dims.kv_max);
+  ctx->kv_dec = bound;
+  return ok();
+}
+
+BM_EXPORT int bm_set_score_accumulation(bm_ctx* ctx, int32_t on) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if (on != 0 && on != 1) return fail(BM_ERR_INVALID_ARG, "score accumulation flag %d", on);
+  ctx->accumulate = on != 0;
+  return ok();
 }
 
 BM_EXPORT int bm_set_decode_removal(bm_ctx* ctx, int32_t p) {
@@ -331,10 +377,28 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
   if (ctx->len > ctx->dims.kv_max)
     return fail(BM_ERR_CAPACITY, "cache holds %d > kv_max=%d entries: evict after the last block",
                 ctx->len, ctx->dims.kv_max);
-  // Algorithm 1's decoding loop taken literally: a full cache first loses p_dec
-  // entries, ranked at the last processed position; the step then only appends
-  if (ctx->p_dec > 0 && ctx->len == ctx->dims.kv_max) {
-    const int st = cut_to(ctx, ctx->dims.kv_max - ctx->p_dec, ctx->last_pos, stream);
+  // The decode bound kd (kv_max unless set lower).  Algorithm 1's decoding loop
+  // taken literally: a cache of kd entries or more first drops to kd - p_dec,
+  // ranked at the last processed position, and the step then only appends.
+  // With one removal per step a cache above kd is first cut to kd.
+  const int kd = ctx->kv_dec;
+  if (ctx->p_dec > kd)
+    return fail(BM_ERR_INVALID_ARG, "decode removal p=%d exceeds the decode bound %d", ctx->p_dec,
+                kd);
+  int target = -1;
+  if (ctx->p_dec > 0 && ctx->len >= kd) target = kd - ctx->p_dec;
+  if (ctx->p_dec == 0 && ctx->len > kd) target = kd;
+  const int len_att = target >= 0 ? target : ctx->len;   // cached entries the step attends to
+  const bool removes = target >= 0 || (ctx->p_dec == 0 && len_att + 1 > kd);
+  if (removes) {
+    const int st = check_rule(ctx);
+    if (st != BM_OK) return st;
+  }
+  if (len_att + 1 > bm::kMaxDecodeLen)
+    return fail(BM_ERR_UNSUPPORTED, "a decode step attends to at most %d entries (%d here)",
+                bm::kMaxDecodeLen, len_att + 1);
+  if (target >= 0) {
+    const int st = cut_to(ctx, target, ctx->last_pos, stream);
     if (st != BM_OK) return st;
   }
   bm::DecodeArgs a;
@@ -352,14 +416,15 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
   a.n_kv_heads = ctx->dims.n_kv_heads;
   a.cap = ctx->cap;
   a.len0 = ctx->len;
-  a.kv_max = ctx->dims.kv_max;
+  a.kv_max = kd;
   a.cur_pos = pos;
   a.units = ctx->units;
+  a.rule = ctx->rule;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
   const hipError_t e =
       bm::launch_decode(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
   if (e != hipSuccess) return hip_fail(e, "decode launch");
-  if (ctx->len < ctx->dims.kv_max) ctx->len += 1;
+  if (ctx->len < kd) ctx->len += 1;
   ctx->next_pos = pos + 1;
   ctx->last_pos = pos;
   return ok();

@@ -19,8 +19,23 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kKeyTile = 64;
-constexpr int kMaxCap = 4096;
+constexpr int kMaxCap = 4096;          // cuts keep up to this many keys in registers
+constexpr int kMaxCapAny = 1 << 16;    // slots per unit (larger cuts stream their keys)
+constexpr int kMaxDecodeLen = 4097;    // entries one decode step attends to (LDS rows)
 constexpr int kMaxBlock = 1024;
+
+// Ranking key of a cut packed with the position into 64 bits, (key bits << 32
+// | pos); every key is >= 0 (scores are sums of probabilities), so the integer
+// order is (key ascending, pos ascending): the smallest key goes first and, on
+// an exact tie, the older entry.
+//   BM_RANK_AVE:    ave = score / (curr_id + 1 - pos), correctly rounded fp32
+//   BM_RANK_SUM:    score
+//   BM_RANK_RECENT: pos alone (the oldest entry goes first)
+__device__ __forceinline__ uint64_t rank_key(int rule, float score, int pos, int curr_id) {
+  if (rule == BM_RANK_RECENT) return (uint64_t)(uint32_t)pos;
+  const float k = rule == BM_RANK_SUM ? score : score / (float)(curr_id + 1 - pos);
+  return ((uint64_t)__float_as_uint(k) << 32) | (uint32_t)pos;
+}
 
 inline int positions_per_wg(int group) { return kWaves * kRowsPerWave / group; }
 
@@ -49,6 +64,7 @@ struct PrefillArgs {
   float* partial;     // [U, npt, cap]
   int64_t seq_ld;
   int n_heads, n_kv_heads, cap, len0, n_tok, t0, npt_used, npt_stride, units;
+  int accumulate;     // 0: outputs only (no score sums; new entries get score 0)
   float scale_log2;   // sm_scale * log2(e)
 };
 
@@ -62,6 +78,7 @@ struct EvictArgs {
   int32_t* srcs;
   int32_t* mcount;
   int cap, n, kv_max, curr_id, units, head_dim, elem_bytes;
+  int rule;           // bm_rank_rule
 };
 
 struct DecodeArgs {
@@ -75,7 +92,8 @@ struct DecodeArgs {
   int32_t* pos;
   int32_t* len;
   int64_t seq_ld;
-  int n_heads, n_kv_heads, cap, len0, kv_max, cur_pos, units;
+  int n_heads, n_kv_heads, cap, len0, kv_max, cur_pos, units;   // kv_max: the decode bound
+  int rule;           // bm_rank_rule
   float scale_log2;
 };
 

@@ -10,8 +10,9 @@
 //      from global memory; f32: VALU dot products);
 //   2. exact softmax per query head (max, sum, normalise) in LDS;
 //   3. score_j += sum_g P[g][j] (the sum_weights update of Sec. 3.2), ranking
-//      key ave = score / (pos_now + 1 - pos) packed with pos into 64 bits, and a
-//      workgroup argmin (older entry first on an exact tie);
+//      key of the chosen rule (by default ave = score / (pos_now + 1 - pos))
+//      packed with pos into 64 bits, and a workgroup argmin (older entry first
+//      on an exact tie);
 //   4. o_g = sum_j P[g][j] v_j on VALU, V rows read once, 16 bytes per lane;
 //   5. write back the scores; if the cache exceeds kv_max, the new pair takes
 //      the slot of the removed entry (or is dropped if it is the one removed);
@@ -28,11 +29,6 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr float kNegInf = -__builtin_huge_valf();
-
-__device__ __forceinline__ uint64_t rank_key(float score, int pos, int curr_id) {
-  const float ave = score / (float)(curr_id + 1 - pos);
-  return ((uint64_t)__float_as_uint(ave) << 32) | (uint32_t)pos;
-}
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int off) {
   const uint32_t lo = __shfl_xor((uint32_t)x, off);
@@ -180,7 +176,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
       const float s = sc[j] + ps;
       sc[j] = s;
-      const uint64_t key = rank_key(s, pos_s[j], a.cur_pos);
+      const uint64_t key = rank_key(a.rule, s, pos_s[j], a.cur_pos);
       if (key < best) {
         best = key;
         bslot = j;

@@ -1,13 +1,14 @@
 // K2 + K3: cut every unit back to kv_max entries and compact in place.
 //
 // K2 (select_kernel), one workgroup per unit: every live entry j gets the
-// ranking key of Sec. 3.2, ave_j = score_j / (curr_id + 1 - pos_j) in IEEE
-// float32 division, packed with its position into one 64-bit integer
-// (ave bits << 32 | pos).  ave >= 0, so the integer order is the order
-// (ave ascending, pos ascending): the smallest ave goes first and, on an exact
-// tie, the older entry (the tie rule of the oracle).  An 8-pass LDS radix
-// select over 8-bit digits finds the E-th smallest key exactly (positions are
-// unique, so exactly E keys are <= it).  Evicted slots below kv_max become
+// ranking key of the chosen rule (by default Sec. 3.2's ave_j = score_j /
+// (curr_id + 1 - pos_j) in IEEE float32 division) packed with its position into
+// one 64-bit integer (rank_key): the integer order is (key ascending, pos
+// ascending), so the smallest key goes first and, on an exact tie, the older
+// entry (the tie rule of the oracle).  An 8-pass LDS radix select over 8-bit
+// digits finds the E-th smallest key exactly (positions are unique, so exactly
+// E keys are <= it).  Up to kMaxCap keys stay in registers; larger caches
+// recompute each key from the scores and positions in every pass.  Evicted slots below kv_max become
 // holes, surviving slots at or above kv_max become sources; both lists are
 // built in slot order with a workgroup prefix count, so the pairing is
 // deterministic.
@@ -20,12 +21,7 @@
 namespace bm {
 namespace {
 
-constexpr int kMaxPer = kMaxCap / 256;  // keys per thread
-
-__device__ __forceinline__ uint64_t rank_key(float score, int pos, int curr_id) {
-  const float ave = score / (float)(curr_id + 1 - pos);
-  return ((uint64_t)__float_as_uint(ave) << 32) | (uint32_t)pos;
-}
+constexpr int kMaxPer = kMaxCap / 256;  // keys per thread held in registers
 
 // exclusive prefix count of `flag` over the workgroup in thread order; returns
 // the workgroup total through *total
@@ -47,6 +43,7 @@ __device__ __forceinline__ int block_excl_count(bool flag, int* s_wave, int* tot
   return before + in_wave;
 }
 
+template <bool STREAM>
 __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
   __shared__ uint32_t hist[256];
   __shared__ uint64_t s_prefix;
@@ -57,13 +54,26 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
   const float* score = a.score + (int64_t)u * a.cap;
   const int32_t* pos = a.pos + (int64_t)u * a.cap;
   const int per = (a.n + 255) / 256;
+  constexpr int KP = STREAM ? 1 : kMaxPer;
 
-  uint64_t key[kMaxPer];
+  uint64_t key[KP];
+  if constexpr (!STREAM) {
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i) {
-    const int j = tid + 256 * i;
-    key[i] = (i < per && j < a.n) ? rank_key(score[j], pos[j], a.curr_id) : ~0ull;
+    for (int i = 0; i < kMaxPer; ++i) {
+      const int j = tid + 256 * i;
+      key[i] = (i < per && j < a.n) ? rank_key(a.rule, score[j], pos[j], a.curr_id) : ~0ull;
+    }
   }
+  // key of entry tid + 256 i (registers, or recomputed when streaming)
+  auto key_of = [&](int i) __device__ -> uint64_t {
+    if constexpr (STREAM) {
+      const int j = tid + 256 * i;
+      return j < a.n ? rank_key(a.rule, score[j], pos[j], a.curr_id) : ~0ull;
+    } else {
+      return key[i];
+    }
+  };
+  const int n_iter = STREAM ? per : kMaxPer;
 
   // radix select of the E-th smallest key (1-based)
   uint64_t prefix = 0;
@@ -74,10 +84,12 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
     hist[tid] = 0;
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kMaxPer; ++i) {
+    for (int i = 0; i < n_iter; ++i) {
       const int j = tid + 256 * i;
-      if (i < per && j < a.n && (key[i] & himask) == prefix)
-        atomicAdd(&hist[(key[i] >> shift) & 255u], 1u);
+      if (i < per && j < a.n) {
+        const uint64_t kk = key_of(i);
+        if ((kk & himask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
+      }
     }
     __syncthreads();
     if (tid < 64) {
@@ -112,11 +124,11 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
   int32_t* srcs = a.srcs + (int64_t)u * a.cap;
   int hbase = 0, sbase = 0;
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i) {
+  for (int i = 0; i < n_iter; ++i) {
     if (i >= per) break;  // uniform across the workgroup
     const int j = tid + 256 * i;
     const bool live = j < a.n;
-    const bool ev = live && key[i] <= thr;
+    const bool ev = live && key_of(i) <= thr;
     const bool is_hole = live && j < a.kv_max && ev;
     const bool is_src = live && j >= a.kv_max && !ev;
     int ht, stot;
@@ -171,7 +183,10 @@ __global__ void __launch_bounds__(256) compact_kernel(EvictArgs a, int nchunks) 
 }  // namespace
 
 hipError_t launch_select(const EvictArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+  if (a.n > kMaxCap)
+    hipLaunchKernelGGL(select_kernel<true>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(select_kernel<false>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

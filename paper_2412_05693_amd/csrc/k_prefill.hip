@@ -509,6 +509,8 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   }
 
   // ======================= sweep 2: exact column sums ========================
+  // (skipped when the caller asked for outputs only)
+  if (!a.accumulate) return;
   // S orientation: lane (n, h) holds key n of a 32-key sub-tile and rows
   // 8i + 4h + j of the wave's 32 rows in accumulator register 4i + j.
   float lse_r[16];
@@ -581,7 +583,8 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 }
 
 // Fold the per-workgroup partial column sums into the scores, in workgroup
-// order: score[j] = (j < len0 ? score[j] : 0) + sum over workgroups that saw j.
+// order: score[j] = (j < len0 ? score[j] : 0) + sum over workgroups that saw j
+// (without accumulation: new entries get 0, older scores stay).
 // Grid: (units, slot chunks of 256); every thread owns one slot and issues its
 // partial-sum loads together.
 __global__ void __launch_bounds__(256) score_reduce_kernel(PrefillArgs a, int pt_positions) {
@@ -593,8 +596,10 @@ __global__ void __launch_bounds__(256) score_reduce_kernel(PrefillArgs a, int pt
     float* score = a.score + (int64_t)u * a.cap;
     const int pt0 = j < a.len0 ? 0 : (j - a.len0) / pt_positions;
     float acc = j < a.len0 ? score[j] : 0.0f;
+    if (a.accumulate) {
 #pragma unroll 8
-    for (int pt = pt0; pt < a.npt_used; ++pt) acc += part[(int64_t)pt * a.cap];
+      for (int pt = pt0; pt < a.npt_used; ++pt) acc += part[(int64_t)pt * a.cap];
+    }
     score[j] = acc;
   }
   if (blockIdx.y == 0 && threadIdx.x == 0) a.len[u] = n;

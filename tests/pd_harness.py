@@ -66,7 +66,7 @@ def _snapshot(pd: PDAttention, units, length):
     return pos, score, dlen
 
 
-def _compare_state(tag, orc, pos, score, dlen, length, st: Stats):
+def _compare_state(tag, orc, pos, score, dlen, length, st: Stats, scores=True):
     if np.any(dlen != length):
         st.fail(f"{tag}: device len {dlen.tolist()} != {length}")
         return False
@@ -77,6 +77,8 @@ def _compare_state(tag, orc, pos, score, dlen, length, st: Stats):
     if not np.array_equal(gpos, opos):
         st.fail(f"{tag}: live positions differ (device {len(gpos)}, oracle {len(opos)})")
         return False
+    if not scores:
+        return True
     err = np.abs(gscore - oscore)
     rel = err / np.maximum(np.abs(oscore), 1e-30)
     st.max_score_rel = max(st.max_score_rel, float(np.max(np.where(err > SCORE_ATOL, rel, 0.0))))
@@ -114,12 +116,16 @@ def _compare_cut(tag, orc: opd.StepOracle, ev, gpu_pos, st: Stats):
 
 
 def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decode_steps=None,
-               inputs=None, pd=None, stop_on_failure=True, decode_p=0) -> Stats:
+               inputs=None, pd=None, stop_on_failure=True, decode_p=0, rule="ave",
+               decode_bound=None, accumulate=True) -> Stats:
     """Run the whole P&D schedule on the device and compare the checked units.
 
     ``decode_p > 0`` selects Algorithm 1's decoding loop taken literally (a step
     that starts with a full cache first removes ``decode_p`` entries); the cut
-    is compared against the device's live set without the step's new entry."""
+    is compared against the device's live set without the step's new entry.
+    ``rule`` is the ranking rule of every cut, ``decode_bound`` the cache bound
+    during decode (default kv_max).  ``accumulate=False`` runs the prefill
+    without score sums: scores are then not compared (only positions)."""
     st = Stats()
     if inputs is None:
         inputs = synth.batch_inputs(wl, device, checked=checked, sharp=sharp)
@@ -128,10 +134,18 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
     pd = pd or make_pd(wl, device)
     if decode_p:
         pd.set_decode_removal(decode_p)
+    if rule != "ave":
+        pd.set_rank_rule(rule)
+    kd = wl.kv_max if decode_bound is None else decode_bound
+    if decode_bound is not None:
+        pd.set_decode_bound(decode_bound)
+    if not accumulate:
+        pd.set_score_accumulation(False)
+    sc = accumulate
     G = wl.group
     uin = {u: synth.unit_inputs(wl, 0, u[0], u[1], sharp=sharp) for u in checked}
     orcs = {u: opd.StepOracle(head_dim=wl.head_dim, group=G, kv_max=wl.kv_max,
-                              sm_scale=wl.sm_scale) for u in checked}
+                              sm_scale=wl.sm_scale, rule=rule) for u in checked}
     tol = OUT_TOL[wl.dtype]
     D = wl.n_decode if decode_steps is None else decode_steps
 
@@ -152,7 +166,8 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
             uq, uk, uv = uin[u]
             ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
             check_out(f"block {t0}", u, slice(t0, t0 + n), ref)
-            _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st)
+            _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st,
+                           sc)
         pd.evict_compact(t0 + n - 1)
         length = pd.length
         pos, score, dlen = _snapshot(pd, checked, length)
@@ -160,7 +175,7 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
             ev = orcs[u].evict(t0 + n - 1, "prefill")
             _compare_cut(f"cut {t0 + n - 1} unit {u}", orcs[u], ev, pos[i], st)
             _compare_state(f"cut {t0 + n - 1} unit {u}", orcs[u], pos[i], score[i], dlen[i],
-                           length, st)
+                           length, st, sc)
         if stop_on_failure and st.failures:
             return st
 
@@ -171,21 +186,23 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
         pos, score, dlen = _snapshot(pd, checked, length)
         for i, u in enumerate(checked):
             uq, uk, uv = uin[u]
+            orc = orcs[u]
             if decode_p:
                 # the oracle's step taken apart (the cut, then append + attend, as in
                 # UnitOracle.decode_step_alg1) so a near-tie cut can be adopted before
                 # the new entry is attended
-                orc = orcs[u]
-                if orc.n == wl.kv_max:
-                    ev = orc.evict(p - 1, "decode", target=wl.kv_max - decode_p)
+                if orc.n >= kd:
+                    ev = orc.evict(p - 1, "decode", target=kd - decode_p)
                     _compare_cut(f"decode {p} unit {u}", orc, ev, pos[i][pos[i] != p], st)
                 orc.append(p, uk[p][None], uv[p][None])
                 ref = orc.attend(uq[:, p][:, None, :], p)[:, 0, :]
             else:
-                ref, ev = orcs[u].decode_step(p, uq[:, p], uk[p], uv[p])
-                _compare_cut(f"decode {p} unit {u}", orcs[u], ev, pos[i], st)
+                if orc.n > kd:    # a lower decode bound: cut first (seen only in the end state)
+                    orc.evict(p - 1, "decode", target=kd)
+                ref, ev = orc.decode_step(p, uq[:, p], uk[p], uv[p], bound=kd)
+                _compare_cut(f"decode {p} unit {u}", orc, ev, pos[i], st)
             check_out(f"decode {p}", u, slice(p, p + 1), ref[:, None, :])
-            _compare_state(f"decode {p} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st)
+            _compare_state(f"decode {p} unit {u}", orc, pos[i], score[i], dlen[i], length, st, sc)
         if stop_on_failure and st.failures:
             return st
     return st

@@ -78,7 +78,7 @@ def test_slots_and_workspace():
     (dict(n_heads=16, n_kv_heads=2), bmx.BM_ERR_UNSUPPORTED),
     (dict(n_heads=6, n_kv_heads=2), bmx.BM_ERR_UNSUPPORTED),
     (dict(block=2048), bmx.BM_ERR_UNSUPPORTED),
-    (dict(kv_max=4000, block=512), bmx.BM_ERR_UNSUPPORTED),
+    (dict(kv_max=65100, block=512), bmx.BM_ERR_UNSUPPORTED),
 ])
 def test_validate_dims_errors(kw, status):
     assert status_of(bmx.bm_validate_dims, dims(**kw)) == status
@@ -191,6 +191,42 @@ def test_decode_removal_range():
     finally:
         bmx.bm_destroy(ctx)
     assert status_of(bmx.bm_set_decode_removal, None, 1) == bmx.BM_ERR_INVALID_ARG
+
+
+def test_rule_bound_and_accumulation_setters():
+    d = dims()
+    ctx = _ctx(d, 128, 520)
+    try:
+        for r in (bmx.BM_RANK_AVE, bmx.BM_RANK_SUM, bmx.BM_RANK_RECENT):
+            bmx.bm_set_rank_rule(ctx, r)
+        assert status_of(bmx.bm_set_rank_rule, ctx, 3) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_set_rank_rule, ctx, -1) == bmx.BM_ERR_INVALID_ARG
+        for bnd in (1, 2, d.kv_max):
+            bmx.bm_set_decode_bound(ctx, bnd)
+        assert status_of(bmx.bm_set_decode_bound, ctx, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_set_decode_bound, ctx, d.kv_max + 1) == bmx.BM_ERR_INVALID_ARG
+        bmx.bm_set_score_accumulation(ctx, 0)
+        bmx.bm_set_score_accumulation(ctx, 1)
+        assert status_of(bmx.bm_set_score_accumulation, ctx, 2) == bmx.BM_ERR_INVALID_ARG
+        assert bmx.bm_ctx_len(ctx) == 128
+    finally:
+        bmx.bm_destroy(ctx)
+    for fn, arg in ((bmx.bm_set_rank_rule, 0), (bmx.bm_set_decode_bound, 1),
+                    (bmx.bm_set_score_accumulation, 1)):
+        assert status_of(fn, None, arg) == bmx.BM_ERR_INVALID_ARG
+
+
+def test_decode_removal_beyond_the_decode_bound_is_rejected_before_launch():
+    d = dims()
+    P = FAKE
+    ctx = _ctx(d, 128, 520)
+    try:
+        bmx.bm_set_decode_bound(ctx, 4)
+        bmx.bm_set_decode_removal(ctx, 5)
+        assert status_of(bmx.bm_decode_step, ctx, 520, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
+        assert bmx.bm_ctx_len(ctx) == 128
+    finally:
+        bmx.bm_destroy(ctx)
 
 
 def test_null_context():

@@ -1,0 +1,104 @@
+"""GPU parity of the other ranking rules and of the comparators of Sec. 4.
+
+* the cumulative sum_weights rule that Sec. 3.2 corrects (BM_RANK_SUM);
+* Algorithm 3, extreme decoding-only eviction (ED): the prompt is processed
+  with no removal and no score sums, then every decode step keeps only the
+  most recent pair (decode bound 2, p = 1, BM_RANK_RECENT) -- at a ragged
+  shape and at the 8192-token prompt of the layer-stack workload, whose first
+  decode cut streams 8192 keys through the select kernel;
+* the full-cache comparator (FKV): bound above s + D, outputs only;
+* a cut of more than 4096 live entries (streaming select) under the paper's
+  rule;
+* the host-side guard against ranking by scores that a block did not add to.
+"""
+import sys
+
+import pytest
+import torch
+
+from paper_2412_05693_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+C2 = synth.WORKLOADS["c2"]
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run(wl, checked, **kw):
+    _need_gpu()
+    from pd_harness import run_parity
+
+    print(f"[parity] {wl.name} dtype={wl.dtype} b={wl.b} H={wl.n_heads}/{wl.n_kv_heads} "
+          f"d={wl.head_dim} s={wl.s} kv={wl.kv_max} B={wl.block} D={wl.n_decode} "
+          f"units={len(checked)} {kw}", flush=True)
+    st = run_parity(wl, checked, **kw)
+    print(f"[parity] -> {st.summary()}", flush=True)
+    sys.stdout.flush()
+    assert not st.failures, "\n".join(st.failures)
+    return st
+
+
+def test_sum_rule_c2_shape():
+    wl = C2.with_(b=2, s=1024, n_decode=24)
+    st = _run(wl, synth.checked_units(wl, wl.units), rule="sum")
+    assert st.cuts == wl.units * (1024 // 256 - 512 // 256 + 24)
+
+
+def test_sum_rule_ragged_fp32_literal_decode():
+    wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, dtype="f32", b=2, n_heads=8,
+                  n_kv_heads=2, head_dim=128, s=200, kv_max=70, block=33, n_decode=9)
+    _run(wl, synth.checked_units(wl, wl.units), rule="sum", decode_p=4)
+
+
+def test_ed_algorithm_3_ragged():
+    wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, b=2, n_heads=8, n_kv_heads=4,
+                  head_dim=64, s=300, kv_max=300, block=48, n_decode=10)
+    st = _run(wl, synth.checked_units(wl, wl.units), rule="recent", decode_bound=2, decode_p=1,
+              accumulate=False)
+    assert st.cuts == wl.units * wl.n_decode
+
+
+def test_ed_algorithm_3_long_prompt():
+    wl = C2.with_(b=1, s=8192, kv_max=8192, block=256, n_decode=4)
+    st = _run(wl, synth.checked_units(wl, 2), rule="recent", decode_bound=2, decode_p=1,
+              accumulate=False)
+    assert st.cuts == 2 * wl.n_decode
+
+
+def test_fkv_outputs_only():
+    wl = C2.with_(b=2, s=600, kv_max=700, block=256, n_decode=10)
+    st = _run(wl, synth.checked_units(wl, wl.units), accumulate=False)
+    assert st.cuts == 0
+
+
+def test_streaming_select_large_cache():
+    # cap = 4512 > 4096 slots: every prefill cut streams its keys
+    wl = C2.with_(b=1, n_heads=4, n_kv_heads=1, s=6000, kv_max=4000, block=512, n_decode=4)
+    st = _run(wl, synth.checked_units(wl, wl.units))
+    assert st.cuts == 5 + 4     # after blocks 7..11 (4096 > 4000 first), then every step
+
+
+def test_unaccumulated_scores_reject_score_ranked_cut():
+    _need_gpu()
+    from pd_harness import make_pd
+    from paper_2412_05693_amd.batchmax import BM_ERR_ORDER, BatchMaxError
+
+    wl = C2.with_(b=1, s=256, kv_max=64, block=128, n_decode=0)
+    q, k, v = synth.batch_inputs(wl, "cuda")
+    o = torch.zeros_like(q)
+    pd = make_pd(wl)
+    pd.set_score_accumulation(False)
+    pd.prefill_block(0, 128, q, k, v, o)
+    with pytest.raises(BatchMaxError) as e:
+        pd.evict_compact(127)
+    assert e.value.status == BM_ERR_ORDER
+    assert pd.length == 128
+    pd.set_rank_rule("recent")
+    pd.evict_compact(127)
+    torch.cuda.synchronize()
+    assert pd.length == 64
+    assert sorted(pd.pos[0, 0, :64].tolist()) == list(range(64, 128))

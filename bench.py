@@ -111,16 +111,19 @@ def _oracle_unit(args):
     with threadpool_limits(1):     # one unit per process, one BLAS thread each
         t = time.perf_counter()
         opd.run_unit(q, k, v, s=wl.s, kv_max=wl.kv_max, block=wl.block, n_decode=wl.n_decode,
-                     sm_scale=wl.sm_scale, p_dec=wl.decode_p)
+                     sm_scale=wl.sm_scale, p_dec=wl.decode_p, rule=wl.rule,
+                     kv_dec=wl.decode_bound or None)
         return time.perf_counter() - t
 
 
-def cpu_baseline(name, overrides, budget_s):
+def cpu_baseline(name, overrides, budget_s, method="bm"):
     """Time the oracle on a sample of units (one per process).  Returns the
     measurement; ``cpu_baseline_line`` scales it to the workload that ran."""
     from paper_2412_05693_amd import synth
 
-    wl = synth.WORKLOADS[name].with_(**overrides)
+    wl = method_workload(synth.WORKLOADS[name].with_(**overrides), method)
+    overrides = dict(overrides, kv_max=wl.kv_max, rule=wl.rule, decode_bound=wl.decode_bound,
+                     decode_p=wl.decode_p, accumulate=wl.accumulate)
     if wl.b == 0:                     # the stack's batch is planned on the GPU later;
         wl = wl.with_(b=64)           # a unit's oracle cost does not depend on b
     cores = len(os.sched_getaffinity(0))
@@ -167,25 +170,61 @@ def cpu_baseline_line(m, wl):
 # ---------------------------------------------------------------------------
 # GPU run
 # ---------------------------------------------------------------------------
+METHODS = {
+    # Batch-Max: bounded cache in prefill and decode (Algorithm 1, Sec. 3.2 rule)
+    "bm": {},
+    # extreme decoding-only eviction (Algorithm 3): full prompt cache, no score
+    # sums, then keep only the most recent pair at every decode step
+    "ed": {"rule": "recent", "decode_bound": 2, "decode_p": 1, "accumulate": False},
+    # full KV cache: nothing is ever removed, no score sums
+    "fkv": {"accumulate": False},
+}
+
+
+def method_workload(wl, method):
+    """The workload as the named method runs it (ED and FKV keep the whole
+    prompt in the cache; FKV also every generated token)."""
+    if method == "ed":
+        return wl.with_(kv_max=max(wl.s, 2), **METHODS["ed"])
+    if method == "fkv":
+        return wl.with_(kv_max=wl.s + wl.n_decode, **METHODS["fkv"])
+    return wl
+
+
+def apply_method(pd, wl):
+    pd.set_decode_removal(wl.decode_p)
+    pd.set_rank_rule(wl.rule)
+    if wl.decode_bound:
+        pd.set_decode_bound(wl.decode_bound)
+    pd.set_score_accumulation(wl.accumulate)
+
+
 def decode_bytes(bmx, wl, b):
     """Algorithmic HBM bytes of all decode launches of one layer: each step at
     the cache length its attention reads (the removal launches of the p > 0
     schedule run inside the timed decode phase but add no bytes here)."""
     es = 4 if wl.dtype == "f32" else 2
     lens = bmx.decode_cache_lengths(s=wl.s, kv_max=wl.kv_max, n_decode=wl.n_decode,
-                                    p=wl.decode_p)
-    return sum(bmx.decode_bytes_per_step(b=b, n_kv_heads=wl.n_kv_heads, group=wl.group,
-                                         head_dim=wl.head_dim, kv_max=n, elem_bytes=es)
-               for n in lens)
+                                    p=wl.decode_p, bound=wl.decode_bound or None)
+    total = 0
+    for n in lens:
+        if n + 1 > bmx.MAX_DECODE_LEN:       # outputs-only split path (no score traffic)
+            total += bmx.decode_bytes_outputs_only(b=b, n_kv_heads=wl.n_kv_heads,
+                                                   group=wl.group, head_dim=wl.head_dim, n=n,
+                                                   elem_bytes=es)
+        else:
+            total += bmx.decode_bytes_per_step(b=b, n_kv_heads=wl.n_kv_heads, group=wl.group,
+                                               head_dim=wl.head_dim, kv_max=n, elem_bytes=es)
+    return total
 
 
-def gpu_bench(name, overrides, steps, warmup):
+def gpu_bench(name, overrides, steps, warmup, method="bm"):
     import torch
 
     from paper_2412_05693_amd import batchmax as bmx
     from paper_2412_05693_amd import synth
 
-    wl = synth.WORKLOADS[name].with_(**overrides)
+    wl = method_workload(synth.WORKLOADS[name].with_(**overrides), method)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     q, k, v = synth.batch_inputs(wl, dev)
@@ -193,7 +232,7 @@ def gpu_bench(name, overrides, steps, warmup):
     pd = bmx.PDAttention(b=wl.b, s=wl.s, kv_max=wl.kv_max, block=wl.block, max_gen=wl.n_decode,
                          n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
                          dtype=wl.dtype, sm_scale=wl.sm_scale, device=dev)
-    pd.set_decode_removal(wl.decode_p)
+    apply_method(pd, wl)
     stream = torch.cuda.current_stream(dev)
     blocks = [(t0, min(wl.block, wl.s - t0)) for t0 in range(0, wl.s, wl.block)]
 
@@ -279,7 +318,7 @@ def gpu_bench(name, overrides, steps, warmup):
 STACK_RESERVE = 3 << 30      # device bytes left to the runtime when planning the batch
 
 
-def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
+def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm"):
     """The layer stack at the largest batch that fits: per (layer, block) the
     device generator writes the block's Q/K/V, then prefill and the cut; then
     the decode steps, layer by layer.  Generator time is measured and left out
@@ -289,7 +328,7 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
     from paper_2412_05693_amd import batchmax as bmx
     from paper_2412_05693_amd import synth
 
-    wl = synth.WORKLOADS[name].with_(**overrides)
+    wl = method_workload(synth.WORKLOADS[name].with_(**overrides), method)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     shape = dict(n_layers=wl.n_layers, s=wl.s, kv_max=wl.kv_max, block=wl.block,
@@ -311,7 +350,7 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None):
                         max_gen=wl.n_decode, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads,
                         head_dim=wl.head_dim, dtype=wl.dtype, sm_scale=wl.sm_scale, device=dev)
     for pd_ in stack.layers:
-        pd_.set_decode_removal(wl.decode_p)
+        apply_method(pd_, wl)
     tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
     H, Hk, d, B = wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.block
     q = torch.empty((b, H, B, d), dtype=tdt, device=dev)
@@ -441,6 +480,10 @@ def main():
     ap.add_argument("--decode-p", type=int, default=0,
                     help="decode removal schedule: 0 = one removal per step (default); p > 0 = "
                          "Algorithm 1's decoding loop, p removals when a step starts full")
+    ap.add_argument("--method", default="bm", choices=sorted(METHODS),
+                    help="bm: Batch-Max (default); ed: Algorithm 3's extreme decoding-only "
+                         "eviction; fkv: full KV cache (the comparators of Sec. 4, run with the "
+                         "same kernels at the largest batch their caches allow)")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -461,11 +504,12 @@ def main():
     overrides = {"decode_p": args.decode_p} if args.decode_p else {}
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args.config, overrides, args.cpu_seconds)
+        cpu = cpu_baseline(args.config, overrides, args.cpu_seconds, args.method)
     if args.config == "c5":
-        res = gpu_bench_stack(args.config, overrides, args.steps, args.warmup, args.batch)
+        res = gpu_bench_stack(args.config, overrides, args.steps, args.warmup, args.batch,
+                              method=args.method)
     else:
-        res = gpu_bench(args.config, overrides, args.steps, args.warmup)
+        res = gpu_bench(args.config, overrides, args.steps, args.warmup, method=args.method)
     wl = res["workload"]
     line = {
         "metric": ("P&D tokens/s (prefill+decode) at max batch; prefill MFMA %, decode HBM GB/s"
@@ -486,6 +530,9 @@ def main():
                    "kv_max": wl.kv_max, "block": wl.block, "decode_steps": wl.n_decode,
                    "decode_removal": (f"{wl.decode_p} at once when full" if wl.decode_p
                                       else "one per step"),
+                   "method": {"bm": "Batch-Max (Algorithm 1)",
+                              "ed": "extreme decoding-only (Algorithm 3)",
+                              "fkv": "full KV cache"}[args.method],
                    "parallelism": "single GPU"},
         "roofline": res["roofline"],
         "cpu_baseline": cpu_baseline_line(cpu, wl) if cpu else None,

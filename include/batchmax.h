@@ -73,8 +73,10 @@ typedef enum bm_rank_rule {
  * p of Algorithm 1), decode steps max_gen, and the attention shape.
  * Supported: head_dim 64 or 128; group n_heads / n_kv_heads of 1, 2 or 4;
  * 1 <= block <= 1024; kv_max >= 1; kv_max + block <= 65536.  A cut of more
- * than 4096 live entries streams its keys from memory (slower); one decode
- * step attends to at most 4097 entries (BM_ERR_UNSUPPORTED beyond). */
+ * than 4096 live entries streams its keys from memory (slower).  A decode
+ * step over more than 4097 entries computes the outputs only (split over key
+ * chunks; the appended entry gets score 0): it needs score accumulation off
+ * and no removal in that step, else BM_ERR_UNSUPPORTED. */
 typedef struct bm_dims {
   int32_t b;
   int32_t s;

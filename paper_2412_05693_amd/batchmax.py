@@ -258,6 +258,9 @@ class PDAttention:
                               self.work_bytes)
         self.units = U
         self.ctx = None
+        # schedule settings (bm_set_*): kept here and applied again to every new
+        # context, so they survive reset() and resume()
+        self._settings = {}
         if init:
             self.reset()
 
@@ -280,15 +283,31 @@ class PDAttention:
         return x.data_ptr() + row * x.shape[3] * x.element_size()
 
     # -- schedule ---------------------------------------------------------------
+    _SETTERS = {"removal": bm_set_decode_removal, "rule": bm_set_rank_rule,
+                "bound": bm_set_decode_bound, "accumulate": bm_set_score_accumulation}
+
+    def _apply_settings(self) -> None:
+        for key, val in self._settings.items():
+            self._SETTERS[key](self.ctx, val)
+
+    def _set(self, key, val) -> None:
+        if self.ctx is not None:
+            self._SETTERS[key](self.ctx, val)   # raises before anything is stored
+        self._settings[key] = val
+
     def reset(self) -> None:
         if self.ctx is not None:
             bm_destroy(self.ctx)
+            self.ctx = None
         self.ctx = bm_init(self.dims, self.cache, self._stream())
+        self._apply_settings()
 
     def resume(self, length: int, next_pos: int) -> None:
         if self.ctx is not None:
             bm_destroy(self.ctx)
+            self.ctx = None
         self.ctx = bm_resume(self.dims, self.cache, length, next_pos)
+        self._apply_settings()
 
     def prefill_block(self, t0, n_tok, q, k, v, o, row=None) -> None:
         row = t0 if row is None else row
@@ -306,20 +325,21 @@ class PDAttention:
     def evict_compact(self, curr_id) -> None:
         bm_evict_compact(self.ctx, curr_id, self._stream())
 
+    # settings persist across reset() and resume()
     def set_decode_removal(self, p: int) -> None:
         """0: one removal per decode step after appending (default); p > 0:
         Algorithm 1's decoding loop, p removals when a step starts full."""
-        bm_set_decode_removal(self.ctx, p)
+        self._set("removal", p)
 
     def set_rank_rule(self, rule) -> None:
         """"ave" (default, Sec. 3.2), "sum" or "recent" (or a BM_RANK_* value)."""
-        bm_set_rank_rule(self.ctx, RANK_RULES.get(rule, rule))
+        self._set("rule", RANK_RULES.get(rule, rule))
 
     def set_decode_bound(self, bound: int) -> None:
-        bm_set_decode_bound(self.ctx, bound)
+        self._set("bound", bound)
 
     def set_score_accumulation(self, on: bool) -> None:
-        bm_set_score_accumulation(self.ctx, 1 if on else 0)
+        self._set("accumulate", 1 if on else 0)
 
     def decode_step(self, pos, q, k, v, o, row=0) -> None:
         H, Hk = self.dims.n_heads, self.dims.n_kv_heads
@@ -521,19 +541,36 @@ def prefill_flops(*, b, n_kv_heads, group, head_dim, s, kv_max, block) -> int:
     return 4 * head_dim * group * total * b * n_kv_heads
 
 
-def decode_cache_lengths(*, s, kv_max, n_decode, p=0) -> list:
+def decode_cache_lengths(*, s, kv_max, n_decode, p=0, bound=None) -> list:
     """Cached entries each decode step's attention reads (before its own pair),
-    under the removal schedule chosen with ``bm_set_decode_removal``: the prompt
-    leaves min(s, kv_max); with p = 0 a step appends then removes one when over
-    the bound; with p > 0 a step that starts full first drops to kv_max - p."""
+    under the removal schedule chosen with ``bm_set_decode_removal`` and the
+    decode bound of ``bm_set_decode_bound`` (default kv_max): the prompt leaves
+    min(s, kv_max); with p = 0 a cache above the bound is cut to it, and a step
+    appends then removes one when over the bound; with p > 0 a step that starts
+    at or above the bound first drops to bound - p."""
+    kd = kv_max if bound is None else bound
     n = min(s, kv_max)
     out = []
     for _ in range(n_decode):
-        if p > 0 and n == kv_max:
-            n = kv_max - p
+        if p > 0 and n >= kd:
+            n = kd - p
+        elif p == 0 and n > kd:
+            n = kd
         out.append(n)
-        n = min(n + 1, kv_max)
+        n = min(n + 1, kd)
     return out
+
+
+MAX_DECODE_LEN = 4097   # entries one step of the scoring decode kernel attends to
+
+
+def decode_bytes_outputs_only(*, b, n_kv_heads, group, head_dim, n, elem_bytes) -> int:
+    """HBM bytes of one outputs-only decode step over n cached entries (the
+    split path past MAX_DECODE_LEN): read n K and V rows, q, the new k and v;
+    write o and append the new K, V row, score and position."""
+    d, G, es = head_dim, group, elem_bytes
+    per_unit = 2 * n * d * es + (G + 2) * d * es + G * d * es + 2 * d * es + 8
+    return per_unit * b * n_kv_heads
 
 
 def decode_bytes_per_step(*, b, n_kv_heads, group, head_dim, kv_max, elem_bytes) -> int:

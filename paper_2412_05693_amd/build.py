@@ -19,7 +19,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libbatchmax.so")
-SOURCES = ["bm_abi.hip", "k_prefill.hip", "k_evict.hip", "k_decode.hip", "k_synth.hip"]
+SOURCES = ["bm_abi.hip", "k_prefill.hip", "k_evict.hip", "k_decode.hip", "k_decode_long.hip",
+           "k_synth.hip"]
 ARCH = "gfx950"
 
 

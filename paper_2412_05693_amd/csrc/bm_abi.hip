@@ -394,9 +394,47 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
     const int st = check_rule(ctx);
     if (st != BM_OK) return st;
   }
-  if (len_att + 1 > bm::kMaxDecodeLen)
-    return fail(BM_ERR_UNSUPPORTED, "a decode step attends to at most %d entries (%d here)",
-                bm::kMaxDecodeLen, len_att + 1);
+  if (len_att + 1 > bm::kMaxDecodeLen) {
+    // outputs only, split over key chunks: the full-cache comparator
+    if (ctx->accumulate || removes)
+      return fail(BM_ERR_UNSUPPORTED,
+                  "a decode step over %d > %d entries computes outputs only: it needs score "
+                  "accumulation off and no removal",
+                  len_att + 1, bm::kMaxDecodeLen);
+    const int nsplit = bm::long_decode_splits(len_att);
+    const size_t need = (size_t)ctx->units * nsplit * ctx->group * (ctx->dims.head_dim + 2);
+    const size_t have = (size_t)ctx->units * ctx->lay.npt * ctx->cap;
+    if (need > have)
+      return fail(BM_ERR_UNSUPPORTED, "workspace too small for a %d-entry decode step",
+                  len_att + 1);
+    bm::LongDecodeArgs a;
+    a.q = q;
+    a.kin = k;
+    a.vin = v;
+    a.o = o;
+    a.kc = ctx->cache.k;
+    a.vc = ctx->cache.v;
+    a.score = ctx->cache.score;
+    a.pos = ctx->cache.pos;
+    a.len = ctx->cache.len;
+    a.part = reinterpret_cast<float*>(work_at(ctx, ctx->lay.partial_off));
+    a.seq_ld = seq_ld;
+    a.n_heads = ctx->dims.n_heads;
+    a.n_kv_heads = ctx->dims.n_kv_heads;
+    a.cap = ctx->cap;
+    a.len0 = ctx->len;
+    a.cur_pos = pos;
+    a.units = ctx->units;
+    a.nsplit = nsplit;
+    a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
+    const hipError_t e =
+        bm::launch_decode_long(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
+    if (e != hipSuccess) return hip_fail(e, "long decode launch");
+    ctx->len += 1;
+    ctx->next_pos = pos + 1;
+    ctx->last_pos = pos;
+    return ok();
+  }
   if (target >= 0) {
     const int st = cut_to(ctx, target, ctx->last_pos, stream);
     if (st != BM_OK) return st;

@@ -97,6 +97,22 @@ struct DecodeArgs {
   float scale_log2;
 };
 
+struct LongDecodeArgs {
+  const void* q;      // [b, H, seq_ld, D] row of this step
+  const void* kin;    // [b, Hk, seq_ld, D]
+  const void* vin;
+  void* o;
+  void* kc;
+  void* vc;
+  float* score;
+  int32_t* pos;
+  int32_t* len;
+  float* part;        // [U][nsplit][G][D + 2] chunk partials (o, m, l)
+  int64_t seq_ld;
+  int n_heads, n_kv_heads, cap, len0, cur_pos, units, nsplit;
+  float scale_log2;
+};
+
 struct SynthArgs {
   void* q;
   void* k;
@@ -114,6 +130,9 @@ hipError_t launch_select(const EvictArgs& a, hipStream_t stream);
 hipError_t launch_compact(const EvictArgs& a, int max_moves, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group,
                          hipStream_t stream);
+int long_decode_splits(int len0);
+hipError_t launch_decode_long(const LongDecodeArgs& a, int dtype, int head_dim, int group,
+                              hipStream_t stream);
 hipError_t launch_reset(float* score, int32_t* len, size_t n_score, size_t n_len,
                         hipStream_t stream);
 hipError_t launch_synth_qkv(const SynthArgs& a, hipStream_t stream);

@@ -66,6 +66,9 @@ class Workload:
     n_layers: int = 1
     seed: int = 1
     decode_p: int = 0     # 0: one removal per decode step; p > 0: Algorithm 1's p at once
+    rule: str = "ave"     # ranking rule of a cut: "ave", "sum" or "recent"
+    decode_bound: int = 0  # cache bound during decode (0: kv_max)
+    accumulate: bool = True  # score sums during prefill
 
     @property
     def group(self) -> int:

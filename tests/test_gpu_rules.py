@@ -6,7 +6,8 @@
   most recent pair (decode bound 2, p = 1, BM_RANK_RECENT) -- at a ragged
   shape and at the 8192-token prompt of the layer-stack workload, whose first
   decode cut streams 8192 keys through the select kernel;
-* the full-cache comparator (FKV): bound above s + D, outputs only;
+* the full-cache comparator (FKV): bound above s + D, outputs only, also
+  with decode steps over more than 4097 entries (the split decode path);
 * a cut of more than 4096 live entries (streaming select) under the paper's
   rule;
 * the host-side guard against ranking by scores that a block did not add to.
@@ -75,6 +76,40 @@ def test_fkv_outputs_only():
     assert st.cuts == 0
 
 
+def test_fkv_long_decode_bf16():
+    # decode steps over 4201..4208 entries: the split outputs-only path
+    wl = C2.with_(b=1, s=4200, kv_max=4208, block=256, n_decode=8)
+    st = _run(wl, synth.checked_units(wl, 2), accumulate=False)
+    assert st.cuts == 0
+
+
+def test_fkv_long_decode_fp32_d64_g2():
+    wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, dtype="f32", b=1, n_heads=4,
+                  n_kv_heads=2, head_dim=64, s=4500, kv_max=4505, block=300, n_decode=5)
+    st = _run(wl, synth.checked_units(wl, wl.units), accumulate=False)
+    assert st.cuts == 0
+
+
+def test_long_decode_needs_outputs_only():
+    _need_gpu()
+    from pd_harness import make_pd
+    from paper_2412_05693_amd.batchmax import BM_ERR_UNSUPPORTED, BatchMaxError
+
+    wl = C2.with_(b=1, s=4200, kv_max=4208, block=512, n_decode=2)
+    q, k, v = synth.batch_inputs(wl, "cuda")
+    o = torch.zeros_like(q)
+    pd = make_pd(wl)
+    for t0 in range(0, wl.s, wl.block):
+        n = min(wl.block, wl.s - t0)
+        pd.prefill_block(t0, n, q, k, v, o)
+        pd.evict_compact(t0 + n - 1)
+    with pytest.raises(BatchMaxError) as e:      # scores on: refused before any launch
+        pd.decode_step(wl.s, q, k, v, o, row=wl.s)
+    assert e.value.status == BM_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert pd.length == wl.s
+
+
 def test_streaming_select_large_cache():
     # cap = 4512 > 4096 slots: every prefill cut streams its keys
     wl = C2.with_(b=1, n_heads=4, n_kv_heads=1, s=6000, kv_max=4000, block=512, n_decode=4)
@@ -92,6 +127,7 @@ def test_unaccumulated_scores_reject_score_ranked_cut():
     o = torch.zeros_like(q)
     pd = make_pd(wl)
     pd.set_score_accumulation(False)
+    pd.reset()                      # settings survive a new context
     pd.prefill_block(0, 128, q, k, v, o)
     with pytest.raises(BatchMaxError) as e:
         pd.evict_compact(127)
@@ -101,4 +137,10 @@ def test_unaccumulated_scores_reject_score_ranked_cut():
     pd.evict_compact(127)
     torch.cuda.synchronize()
     assert pd.length == 64
+    assert sorted(pd.pos[0, 0, :64].tolist()) == list(range(64, 128))
+    # both settings again after a reset: accumulation still off, rule still recent
+    pd.reset()
+    pd.prefill_block(0, 128, q, k, v, o)
+    pd.evict_compact(127)
+    torch.cuda.synchronize()
     assert sorted(pd.pos[0, 0, :64].tolist()) == list(range(64, 128))

@@ -60,6 +60,7 @@ class UnitOracle:
     kv_max: int         # the paper's maximum cache size |kv|-bar
     sm_scale: float
     rule: str = "ave"   # ranking key of a cut, see ``ranking_key``
+    pad: int = 0        # left pad tokens of the unit's sample (Sec. 3), reading R11
     pos: np.ndarray = field(default=None)
     k: np.ndarray = field(default=None)
     v: np.ndarray = field(default=None)
@@ -103,21 +104,31 @@ class UnitOracle:
         ``sum_weights += sum_i attn_weights[i]`` over every query of the block
         and every query head of the group (Sec. 3.2 update; reading R7).
         Returns the attention outputs ``[G, m, d]``.
+
+        Left padding (Sec. 3, reading R11): the ``pad`` first positions of the
+        sample are pad tokens.  Their keys are visible to no query (they keep
+        score 0), and a pad query attends to nothing: its output is zero and it
+        adds nothing to any score.
         """
         q = np.asarray(q, dtype=np.float64)
         g_heads, m, d = q.shape
         qpos = first_pos + np.arange(m, dtype=np.int64)
-        visible = self.pos[None, :] <= qpos[:, None]                  # [m, n]
+        real_q = qpos >= self.pad
+        visible = (self.pos[None, :] <= qpos[:, None]) & (self.pos[None, :] >= self.pad)
+        visible &= real_q[:, None]                                     # [m, n]
         out = np.zeros((g_heads, m, d))
         for g in range(g_heads):
             logits = self.sm_scale * (q[g] @ self.k.T)                # [m, n]
             logits = np.where(visible, logits, -np.inf)
-            logits = logits - logits.max(axis=1, keepdims=True)
-            w = np.exp(logits)
-            p = w / w.sum(axis=1, keepdims=True)                       # rows sum to 1
+            p = np.zeros_like(logits)
+            if real_q.any():
+                z = logits[real_q]
+                z = z - z.max(axis=1, keepdims=True)
+                w = np.exp(z)
+                p[real_q] = w / w.sum(axis=1, keepdims=True)           # real rows sum to 1
             out[g] = p @ self.v
             self.score = self.score + p.sum(axis=0)
-        self.queries_seen += g_heads * m
+        self.queries_seen += g_heads * int(real_q.sum())
         return out
 
     # -- eviction rule ------------------------------------------------------------
@@ -271,7 +282,7 @@ class Trace:
 
 def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
              sm_scale: float, p_dec: int = 0, rule: str = "ave",
-             kv_dec: int | None = None) -> Trace:
+             kv_dec: int | None = None, pad: int = 0) -> Trace:
     """Full P&D run of one unit (Sec. 3.1, Algorithm 1 under reading R1).
 
     ``q`` is ``[G, s + n_decode, d]``; ``k``, ``v`` are ``[s + n_decode, d]``,
@@ -288,13 +299,15 @@ def run_unit(q, k, v, *, s: int, kv_max: int, block: int, n_decode: int,
     cache larger than ``kv_dec`` at the first step is first cut to ``kv_dec``
     with curr_id = the last processed position.  Algorithm 3 (ED): ``kv_max >=
     s`` (no removal while prefilling), ``kv_dec = 2``, ``p_dec = 1``,
-    ``rule = "recent"``.
+    ``rule = "recent"``.  ``pad`` left pad tokens occupy positions 0..pad-1
+    of the prompt (Sec. 3; see ``UnitOracle.attend``).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     g_heads, total, d = q.shape
-    unit = UnitOracle(head_dim=d, group=g_heads, kv_max=kv_max, sm_scale=sm_scale, rule=rule)
+    unit = UnitOracle(head_dim=d, group=g_heads, kv_max=kv_max, sm_scale=sm_scale, rule=rule,
+                      pad=pad)
     kd = kv_max if kv_dec is None else kv_dec
     out = np.zeros((g_heads, total, d))
     events = []

@@ -354,9 +354,76 @@ def pin_alg3_closed_form(cls):
     assert sorted(int(p) for p in u.pos) == [s + D - 2, s + D - 1]
 
 
+def _run_padded(cls, q, k, v, *, s, kv_max, block, n_decode, sm_scale, pad):
+    G, T, d = q.shape
+    u = cls(head_dim=d, group=G, kv_max=kv_max, sm_scale=sm_scale, pad=pad)
+    out = np.zeros((G, T, d))
+    events = []
+    for t0 in range(0, s, block):
+        t1 = min(s, t0 + block)
+        out[:, t0:t1] = u.prefill_block(t0, q[:, t0:t1], k[t0:t1], v[t0:t1])
+        ev = u.evict(t1 - 1, "prefill")
+        if ev is not None:
+            events.append(ev)
+    for t in range(n_decode):
+        i = s + t
+        out[:, i], ev = u.decode_step(i, q[:, i], k[i], v[i])
+        if ev is not None:
+            events.append(ev)
+    return out, events, u
+
+
+def pin_left_padding_is_a_shift(cls):
+    """Left padding by a multiple of the block (Sec. 3): the real tokens' outputs,
+    every cut that removes a real entry, and the final cache equal those of the
+    unpadded run of the same real tokens, shifted by the pad; pad vectors are
+    large junk, so a pad key that leaked into any softmax would show."""
+    rng = np.random.default_rng(53)
+    for (G, s_real, D, d, kv, B, n_blocks_pad) in [(2, 24, 5, 8, 6, 4, 2), (1, 18, 4, 4, 5, 3, 3)]:
+        pad = n_blocks_pad * B
+        q, k, v = _rand_unit(rng, G, s_real + D, d)
+        ref, rev, ru = _run(cls, q, k, v, s=s_real, kv_max=kv, block=B, n_decode=D, sm_scale=0.6)
+        jq = rng.standard_normal((G, pad, d)) * 30.0
+        jk = rng.standard_normal((pad, d)) * 30.0
+        jv = rng.standard_normal((pad, d)) * 30.0
+        qp = np.concatenate([jq, q], axis=1)
+        kp, vp = np.concatenate([jk, k]), np.concatenate([jv, v])
+        out, ev, u = _run_padded(cls, qp, kp, vp, s=pad + s_real, kv_max=kv, block=B,
+                                 n_decode=D, sm_scale=0.6, pad=pad)
+        np.testing.assert_allclose(out[:, pad:], ref, rtol=0, atol=1e-12)
+        assert not out[:, :pad].any()
+        real_cuts = [list(e.kept_pos) for e in ev if any(p >= pad for p in e.evicted_pos)]
+        assert real_cuts == [[p + pad for p in e.kept_pos] for e in rev]
+        order, rorder = np.argsort(u.pos), np.argsort(ru.pos)
+        assert list(u.pos[order]) == [p + pad for p in ru.pos[rorder]]
+        np.testing.assert_allclose(u.score[order], ru.score[rorder], rtol=0, atol=1e-12)
+
+
+def pin_left_padding_invariants(cls):
+    """Any left pad: pad rows give zero outputs, pad keys keep score 0 and are
+    removed before any real entry (ave 0, older), and the scores of the live
+    and removed entries add up to G per real query."""
+    rng = np.random.default_rng(59)
+    G, s, D, d, kv, B, pad = 2, 23, 4, 6, 5, 4, 7
+    q, k, v = _rand_unit(rng, G, s + D, d)
+    out, ev, u = _run_padded(cls, q, k, v, s=s, kv_max=kv, block=B, n_decode=D, sm_scale=0.7,
+                             pad=pad)
+    assert not out[:, :pad].any()
+    for e in ev:
+        pads_kept = [p for p in e.kept_pos if p < pad]
+        real_removed = [p for p in e.evicted_pos if p >= pad]
+        assert not (pads_kept and real_removed)
+        for p, sc in zip(e.all_pos, e.all_score):
+            if p < pad:
+                assert sc == 0.0
+    total = float(u.score.sum()) + u.evicted_score_total
+    assert abs(total - G * (s + D - pad)) < 1e-9
+
+
 ALL_PINS = [pin_dense_fixed_point, pin_golden, pin_selection_bruteforce,
             pin_conservation_and_lengths, pin_paper_stated_values, pin_permutation_invariance,
-            pin_micro_agreement, pin_super_key, pin_rule_keys_bruteforce, pin_alg3_closed_form]
+            pin_micro_agreement, pin_super_key, pin_rule_keys_bruteforce, pin_alg3_closed_form,
+            pin_left_padding_is_a_shift, pin_left_padding_invariants]
 
 
 @pytest.mark.parametrize("pin", ALL_PINS, ids=lambda f: f.__name__)
@@ -503,9 +570,32 @@ class _RecentKeepsOldest(opd.StepOracle):
         return super().ranking_key(curr_id)
 
 
+class _PadKeysVisible(opd.StepOracle):
+    def attend(self, q, first_pos):
+        saved = self.pad
+        self.pad = 0
+        try:
+            return super().attend(q, first_pos)
+        finally:
+            self.pad = saved
+
+
+class _PadQueriesScore(opd.StepOracle):
+    def attend(self, q, first_pos):
+        out = super().attend(q, first_pos)
+        q = np.asarray(q)
+        m = q.shape[1]
+        n_pad_rows = int(np.clip(self.pad - first_pos, 0, m))
+        if n_pad_rows and self.n:
+            # each pad row spreads its weight uniformly over the visible keys
+            self.score = self.score + q.shape[0] * n_pad_rows / self.n
+        return out
+
+
 @pytest.mark.parametrize("mutant", [_DenomOffByOne, _NoSelfAttention, _TieNewestFirst,
                                     _FirstHeadOnly, _NoScale, _TransposedValues, _EvictLargest,
-                                    _SumRuleUsesAverages, _RecentKeepsOldest],
+                                    _SumRuleUsesAverages, _RecentKeepsOldest, _PadKeysVisible,
+                                    _PadQueriesScore],
                          ids=lambda c: c.__name__)
 def test_planted_mistake_is_caught(mutant):
     failures = 0

@@ -112,7 +112,7 @@ def _oracle_unit(args):
         t = time.perf_counter()
         opd.run_unit(q, k, v, s=wl.s, kv_max=wl.kv_max, block=wl.block, n_decode=wl.n_decode,
                      sm_scale=wl.sm_scale, p_dec=wl.decode_p, rule=wl.rule,
-                     kv_dec=wl.decode_bound or None)
+                     kv_dec=wl.decode_bound or None, pad=int(synth.sample_pads(wl)[bi]))
         return time.perf_counter() - t
 
 
@@ -158,7 +158,9 @@ def cpu_baseline_line(m, wl):
     all units, spread over the same number of processes."""
     total_units = wl.units * wl.n_layers
     t_full = m["per_unit_s"] * total_units / m["cores"]
-    tok = wl.b * (wl.s + wl.n_decode)
+    from paper_2412_05693_amd import synth
+
+    tok = wl.b * (wl.s + wl.n_decode) - int(synth.sample_pads(wl).sum())
     what = "(layer, sample, KV head)" if wl.n_layers > 1 else "(sample, KV head)"
     return {"value": tok / t_full, "unit": "tokens/s", "cores": m["cores"], "kind": "oracle",
             "sample": f"{m['done']} {what} units of {wl.name}, full P&D each, float64 numpy, "
@@ -233,6 +235,9 @@ def gpu_bench(name, overrides, steps, warmup, method="bm"):
                          n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
                          dtype=wl.dtype, sm_scale=wl.sm_scale, device=dev)
     apply_method(pd, wl)
+    pads = synth.sample_pads(wl)
+    if wl.pad_max > 0:
+        pd.set_left_padding(torch.from_numpy(pads).to(dev))
     stream = torch.cuda.current_stream(dev)
     blocks = [(t0, min(wl.block, wl.s - t0)) for t0 in range(0, wl.s, wl.block)]
 
@@ -278,8 +283,13 @@ def gpu_bench(name, overrides, steps, warmup, method="bm"):
 
     G = wl.group
     es = 4 if wl.dtype == "f32" else 2
-    flops = bmx.prefill_flops(b=wl.b, n_kv_heads=wl.n_kv_heads, group=G, head_dim=wl.head_dim,
-                              s=wl.s, kv_max=wl.kv_max, block=wl.block)
+    if wl.pad_max > 0:
+        flops = bmx.prefill_flops_padded(pads=pads, n_kv_heads=wl.n_kv_heads, group=G,
+                                         head_dim=wl.head_dim, s=wl.s, kv_max=wl.kv_max,
+                                         block=wl.block)
+    else:
+        flops = bmx.prefill_flops(b=wl.b, n_kv_heads=wl.n_kv_heads, group=G,
+                                  head_dim=wl.head_dim, s=wl.s, kv_max=wl.kv_max, block=wl.block)
     dbytes = decode_bytes(bmx, wl, wl.b)
     peak_f = PEAK_F32_MFMA if wl.dtype == "f32" else PEAK_BF16_MFMA
     prefill_tflops = flops / (pf_ms * 1e-3) / 1e12
@@ -302,13 +312,14 @@ def gpu_bench(name, overrides, steps, warmup, method="bm"):
     roofline = {"bound": kd["bound"], "achieved": round(kd["achieved"], 3), "peak": kd["peak"],
                 "unit": kd["unit"], "frac": round(kd["frac"], 5), "traffic": traffic,
                 "kernel": dom}
-    tokens = wl.b * (wl.s + wl.n_decode)
+    prompt_tokens = int(wl.b * wl.s - pads.sum())        # real tokens only (Sec. 3 padding)
+    tokens = prompt_tokens + wl.b * wl.n_decode
     return {
         "value": tokens / (ms_step * 1e-3),
         "ms_per_step": ms_step,
         "roofline": roofline,
         "kernels": kernels,
-        "phases": {"prefill_tokens_per_s": wl.b * wl.s / ((pf_ms + ev_ms) * 1e-3),
+        "phases": {"prefill_tokens_per_s": prompt_tokens / ((pf_ms + ev_ms) * 1e-3),
                    "decode_tokens_per_s": (wl.b * wl.n_decode / (dec_ms * 1e-3)
                                            if wl.n_decode else None)},
         "workload": wl,
@@ -484,6 +495,9 @@ def main():
                     help="bm: Batch-Max (default); ed: Algorithm 3's extreme decoding-only "
                          "eviction; fkv: full KV cache (the comparators of Sec. 4, run with the "
                          "same kernels at the largest batch their caches allow)")
+    ap.add_argument("--pad-max", type=int, default=0,
+                    help="single-layer workloads: left-pad sample j by pad_j in [0, N] tokens "
+                         "(per-sample prompt lengths s - pad_j, Sec. 3); value counts real tokens")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -502,6 +516,11 @@ def main():
         sys.exit(2)
 
     overrides = {"decode_p": args.decode_p} if args.decode_p else {}
+    if args.pad_max:
+        if args.config == "c5":
+            print("bench.py: --pad-max applies to the single-layer workloads", file=sys.stderr)
+            sys.exit(2)
+        overrides["pad_max"] = args.pad_max
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, overrides, args.cpu_seconds, args.method)
@@ -530,6 +549,7 @@ def main():
                    "kv_max": wl.kv_max, "block": wl.block, "decode_steps": wl.n_decode,
                    "decode_removal": (f"{wl.decode_p} at once when full" if wl.decode_p
                                       else "one per step"),
+                   "left_pad_max": wl.pad_max,
                    "method": {"bm": "Batch-Max (Algorithm 1)",
                               "ed": "extreme decoding-only (Algorithm 3)",
                               "fkv": "full KV cache"}[args.method],

@@ -201,6 +201,17 @@ int bm_set_rank_rule(bm_ctx* ctx, int32_t rule);
  * BM_RANK_RECENT.  A decode step with p > bound returns BM_ERR_INVALID_ARG. */
 int bm_set_decode_bound(bm_ctx* ctx, int32_t bound);
 
+/* Left padding (Sec. 3): pad points at b int32 values on the device (caller-
+ * owned, alive while work is enqueued), pad[j] = s - s_j, the number of pad
+ * tokens in front of sample j's prompt; null (the default) means none.  Pad
+ * tokens occupy positions 0 .. pad[j]-1 and are processed like any token, but
+ * their keys are visible to no query (their scores stay 0, so every cut
+ * removes them first) and a pad query attends to nothing: its output is 0
+ * and it adds to no score.  Values below 0 count as 0.  Set it before the
+ * first prefill block and keep it for the whole run (a context rebuilt with
+ * bm_resume needs it again); 4-byte aligned, else BM_ERR_INVALID_ARG. */
+int bm_set_left_padding(bm_ctx* ctx, const int32_t* pad);
+
 /* Score accumulation during prefill (default on = 1).  Off (0): later
  * bm_prefill_block calls compute the attention outputs only (new entries get
  * score 0), the prefill of the full-cache and decoding-only comparators of

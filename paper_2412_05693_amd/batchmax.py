@@ -83,6 +83,7 @@ def _load() -> ctypes.CDLL:
         "bm_set_rank_rule": (ctypes.c_int, [P, I32]),
         "bm_set_decode_bound": (ctypes.c_int, [P, I32]),
         "bm_set_score_accumulation": (ctypes.c_int, [P, I32]),
+        "bm_set_left_padding": (ctypes.c_int, [P, P]),
         "bm_decode_step": (ctypes.c_int, [P, I32, P, P, P, P, I32, P]),
         "bm_ctx_len": (I32, [P]),
         "bm_ctx_next_pos": (I32, [P]),
@@ -101,7 +102,7 @@ _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
             "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block", "bm_evict_compact",
             "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
-            "bm_set_score_accumulation",
+            "bm_set_score_accumulation", "bm_set_left_padding",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
             "bm_philox4x32_10")
 
@@ -170,6 +171,10 @@ def bm_set_decode_bound(ctx: int, bound: int) -> None:
 
 def bm_set_score_accumulation(ctx: int, on: int) -> None:
     _check(_lib.bm_set_score_accumulation(ctx, on))
+
+
+def bm_set_left_padding(ctx: int, pad_ptr: int) -> None:
+    _check(_lib.bm_set_left_padding(ctx, pad_ptr))
 
 
 def bm_decode_step(ctx: int, pos: int, q: int, k: int, v: int, o: int, seq_ld: int,
@@ -284,7 +289,8 @@ class PDAttention:
 
     # -- schedule ---------------------------------------------------------------
     _SETTERS = {"removal": bm_set_decode_removal, "rule": bm_set_rank_rule,
-                "bound": bm_set_decode_bound, "accumulate": bm_set_score_accumulation}
+                "bound": bm_set_decode_bound, "accumulate": bm_set_score_accumulation,
+                "pad": bm_set_left_padding}
 
     def _apply_settings(self) -> None:
         for key, val in self._settings.items():
@@ -340,6 +346,20 @@ class PDAttention:
 
     def set_score_accumulation(self, on: bool) -> None:
         self._set("accumulate", 1 if on else 0)
+
+    def set_left_padding(self, pads) -> None:
+        """Left pad tokens per sample: a contiguous int32 tensor of b values on
+        the device (kept referenced here), or None for no padding."""
+        if pads is None:
+            self._pads = None
+            self._set("pad", None)
+            return
+        t = self.torch
+        if pads.dtype != t.int32 or pads.device != self.device or not pads.is_contiguous() or \
+                tuple(pads.shape) != (self.dims.b,):
+            raise ValueError(f"pads: need a contiguous int32 [{self.dims.b}] tensor on {self.device}")
+        self._pads = pads
+        self._set("pad", pads.data_ptr())
 
     def decode_step(self, pos, q, k, v, o, row=0) -> None:
         H, Hk = self.dims.n_heads, self.dims.n_kv_heads
@@ -529,6 +549,28 @@ def plan_stack_batch(budget_bytes: int, **shape) -> int:
 # ---------------------------------------------------------------------------
 # algorithmic work (used by the benchmark's roofline figures)
 # ---------------------------------------------------------------------------
+def prefill_flops_padded(*, pads, n_kv_heads, group, head_dim, s, kv_max, block) -> int:
+    """prefill_flops with left padding (Sec. 3): only real queries and the real
+    keys they see count.  Pads are removed before any real entry, so after a
+    cut the cache holds min(real so far, kv_max) real entries."""
+    total = 0
+    for p in (int(x) for x in pads):
+        real = pad = 0                     # entries in the cache
+        for t0 in range(0, s, block):
+            t1 = min(s, t0 + block)
+            r0 = max(p, t0)                # first real row of the block
+            n = max(0, t1 - r0)
+            total += n * real + n * (n + 1) // 2
+            real += n
+            pad += (t1 - t0) - n
+            excess = real + pad - kv_max
+            if excess > 0:
+                drop = min(pad, excess)
+                pad -= drop
+                real -= excess - drop
+    return total * 4 * head_dim * group * n_kv_heads
+
+
 def prefill_flops(*, b, n_kv_heads, group, head_dim, s, kv_max, block) -> int:
     """QK^T + PV flops the method must do: 4 d G per visible (query, key) pair."""
     total = 0

@@ -29,6 +29,7 @@ struct bm_ctx {
   int32_t rule;       // bm_rank_rule of every cut
   bool accumulate;    // prefill adds probabilities to the scores
   bool scores_valid;  // no block has run without accumulation
+  const int32_t* pad; // device [b] left pad tokens per sample, or null
 };
 
 namespace {
@@ -170,6 +171,7 @@ int make_ctx(const bm_dims* dims, const bm_cache* cache, bm_ctx** out) {
   c->rule = BM_RANK_AVE;
   c->accumulate = true;
   c->scores_valid = true;
+  c->pad = nullptr;
   *out = c;
   return BM_OK;
 }
@@ -257,6 +259,7 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   a.npt_stride = ctx->lay.npt;
   a.units = ctx->units;
   a.accumulate = ctx->accumulate ? 1 : 0;
+  a.pad = ctx->pad;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
   hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
@@ -343,6 +346,13 @@ BM_EXPORT int bm_set_decode_bound(bm_ctx* ctx, int32_t bound) {
   return ok();
 }
 
+BM_EXPORT int bm_set_left_padding(bm_ctx* ctx, const int32_t* pad) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  if ((uintptr_t)pad & 3) return fail(BM_ERR_INVALID_ARG, "pad must be 4-byte aligned");
+  ctx->pad = pad;
+  return ok();
+}
+
 BM_EXPORT int bm_set_score_accumulation(bm_ctx* ctx, int32_t on) {
   if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
   if (on != 0 && on != 1) return fail(BM_ERR_INVALID_ARG, "score accumulation flag %d", on);
@@ -426,6 +436,7 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
     a.cur_pos = pos;
     a.units = ctx->units;
     a.nsplit = nsplit;
+    a.pad = ctx->pad;
     a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
     const hipError_t e =
         bm::launch_decode_long(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
@@ -458,6 +469,7 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
   a.cur_pos = pos;
   a.units = ctx->units;
   a.rule = ctx->rule;
+  a.pad = ctx->pad;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
   const hipError_t e =
       bm::launch_decode(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);

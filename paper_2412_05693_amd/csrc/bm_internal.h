@@ -65,6 +65,7 @@ struct PrefillArgs {
   int64_t seq_ld;
   int n_heads, n_kv_heads, cap, len0, n_tok, t0, npt_used, npt_stride, units;
   int accumulate;     // 0: outputs only (no score sums; new entries get score 0)
+  const int32_t* pad; // [b] left pad tokens per sample, or null
   float scale_log2;   // sm_scale * log2(e)
 };
 
@@ -94,6 +95,7 @@ struct DecodeArgs {
   int64_t seq_ld;
   int n_heads, n_kv_heads, cap, len0, kv_max, cur_pos, units;   // kv_max: the decode bound
   int rule;           // bm_rank_rule
+  const int32_t* pad; // [b] left pad tokens per sample, or null
   float scale_log2;
 };
 
@@ -110,6 +112,7 @@ struct LongDecodeArgs {
   float* part;        // [U][nsplit][G][D + 2] chunk partials (o, m, l)
   int64_t seq_ld;
   int n_heads, n_kv_heads, cap, len0, cur_pos, units, nsplit;
+  const int32_t* pad; // [b] left pad tokens per sample, or null
   float scale_log2;
 };
 

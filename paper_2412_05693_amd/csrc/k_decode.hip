@@ -146,10 +146,19 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   }
 
   // ---------------- 2. softmax per query head ----------------
+  // (left padding: pad entries, pos < pad, are visible to no query)
+  const int pad = a.pad ? max(0, a.pad[bi]) : 0;
   for (int g = w; g < G; g += 4) {
     float* pg = P + g * Lp;
     float m = kNegInf;
-    for (int j = lane; j < L; j += 64) m = fmaxf(m, pg[j]);
+    for (int j = lane; j < L; j += 64) {
+      float x = pg[j];
+      if (pad > 0 && pos_s[j] < pad) {
+        x = kNegInf;
+        pg[j] = x;
+      }
+      m = fmaxf(m, x);
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     float s = 0.0f;

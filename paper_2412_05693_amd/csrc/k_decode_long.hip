@@ -79,6 +79,7 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
   __syncthreads();
 
   const int r_in = lane / CPR, ch = lane - r_in * CPR;
+  const int pad = a.pad ? max(0, a.pad[bi]) : 0;
   // 1. logits: wave w takes row groups w, w + 4, ... of the chunk
   for (int base = w * RPL; base < nj; base += 4 * RPL) {
     const int r = base + r_in;
@@ -100,8 +101,10 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
 #pragma unroll
       for (int g = 0; g < G; ++g) part[g] += __shfl_xor(part[g], off);
     if (ch == 0 && r < nj) {
+      // left padding: a pad entry (pos < pad) is visible to no query
+      const bool masked = pad > 0 && j < a.len0 && a.pos[(int64_t)u * a.cap + j] < pad;
 #pragma unroll
-      for (int g = 0; g < G; ++g) z[g][r] = part[g];
+      for (int g = 0; g < G; ++g) z[g][r] = masked ? kNegInf : part[g];
     }
   }
   __syncthreads();
@@ -114,7 +117,8 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
     for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     float l = 0.0f;
     for (int r = lane; r < nj; r += 64) {
-      const float p = __builtin_amdgcn_exp2f(z[w][r] - m);
+      // a chunk of pad entries only: no weight (m = -inf)
+      const float p = m == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(z[w][r] - m);
       z[w][r] = p;
       l += p;
     }
@@ -190,7 +194,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(LongDecodeArgs a) {
     float num = 0.0f, den = 0.0f;
     for (int c = 0; c < a.nsplit; ++c) {
       const float* pc = part + (c * G + g) * (D + 2);
-      const float f = __builtin_amdgcn_exp2f(pc[D] - M);
+      const float f = pc[D] == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(pc[D] - M);
       num = fmaf(f, pc[e], num);
       den = fmaf(f, pc[D + 1], den);
     }

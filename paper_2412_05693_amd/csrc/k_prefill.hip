@@ -133,9 +133,11 @@ struct Geo {
   bool wave_active;
   int in_rows;     // block rows the workgroup reads: min(n_tok, pbase + PT)
   int ntc, nt;     // cache tiles, all tiles
+  int pad;         // left pad tokens of the sample (positions < pad are pads)
+  bool qpad;       // this lane's query row is a pad token
 };
 
-template <int G>
+template <int G, bool PAD>
 __device__ __forceinline__ Geo make_geo(const PrefillArgs& a) {
   Geo s;
   // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
@@ -164,6 +166,8 @@ __device__ __forceinline__ Geo make_geo(const PrefillArgs& a) {
   s.in_rows = min(a.n_tok, s.pbase + PT);
   s.ntc = (a.len0 + kKeyTile - 1) / kKeyTile;
   s.nt = s.ntc + (s.in_rows + kKeyTile - 1) / kKeyTile;
+  s.pad = PAD ? max(0, a.pad[s.bi]) : 0;
+  s.qpad = a.t0 + s.row < s.pad;
   return s;
 }
 
@@ -188,8 +192,11 @@ __device__ __forceinline__ TileInfo tile_info(const PrefillArgs& a, const Geo& s
 __device__ __forceinline__ bool tile_active(const Geo& s, const TileInfo& ti) {
   return s.wave_active && (ti.cache || ti.base <= s.wlast);
 }
-__device__ __forceinline__ bool tile_masked(const Geo& s, const TileInfo& ti) {
-  return ti.cache ? ti.valid < kKeyTile : ti.base + kKeyTile - 1 > s.wrow0;
+__device__ __forceinline__ bool tile_masked(const PrefillArgs& a, const Geo& s,
+                                            const TileInfo& ti) {
+  // left padding: cache tiles may hold pad entries; block tiles below the pad
+  const bool pads = s.pad > 0 && (ti.cache || a.t0 + ti.base < s.pad);
+  return pads || (ti.cache ? ti.valid < kKeyTile : ti.base + kKeyTile - 1 > s.wrow0);
 }
 
 // Tiles of K (rows in kappa order) and V are copied into LDS with buffer loads
@@ -226,8 +233,10 @@ __device__ __forceinline__ void dma_rows(char* dst, const TileSrc& src, const Ti
   }
 }
 
-template <bool BF16, int D, int G>
+template <bool BF16, int D, int G, bool PAD>
 __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_attn_kernel(PrefillArgs a) {
+  // PAD: the launch has left padding (a separate instantiation, so the common
+  // case carries none of its registers)
   using C = Cfg<BF16, D>;
   using E = typename C::E;
   constexpr int RB = C::RB;
@@ -239,7 +248,10 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   __shared__ __attribute__((aligned(1024))) char vb1[C::V_BYTES];
   __shared__ float cs0[kWaves][kKeyTile];
   __shared__ float cs1[kWaves][kKeyTile];
-  const Geo s = make_geo<G>(a);
+  // positions of the cached keys of tile t in pk_ring[t % 3] (left padding
+  // only): tile t's positions are read while tile t + 2's are being fetched
+  __shared__ int32_t pk_ring[3][kKeyTile];
+  const Geo s = make_geo<G, PAD>(a);
   const int tid = threadIdx.x;
 
   // ---- append the workgroup's block rows to the cache tail (Sec. 3.2: new
@@ -277,8 +289,27 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     r.rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nrec, kRsrcWord3);
     return r;
   };
-  auto dma_k = [&](char* dst, const TileInfo& ti) __device__ {
+  const uint64_t pos_base = (uint64_t)(a.pos + (int64_t)s.u * a.cap);
+  auto dma_k = [&](char* dst, const TileInfo& ti, int t) __device__ {
     dma_rows<BF16, D, true>(dst, tile_src(ti, true), ti, s);
+    if (PAD && s.pad > 0 && ti.cache && s.w == 0) {
+      // the tile's key positions, in key order, next to the K rows
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)pos_base);
+      const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(pos_base >> 32));
+      const int nrec = __builtin_amdgcn_readfirstlane(a.len0 * 4);
+      const __amdgpu_buffer_rsrc_t r =
+          __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nrec, kRsrcWord3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)pk_ring[t % 3], 4,
+                                               (ti.base + s.lane) * 4, 0, 0, 0);
+    }
+  };
+  // bit k set: key k of tile ti is a pad token (cache keys through the LDS copy
+  // of their positions); uniform across the workgroup
+  auto pad_bits = [&](const TileInfo& ti, const int32_t* pk) __device__ -> uint64_t {
+    if (!PAD || s.pad == 0) return 0;
+    if (ti.cache) return __ballot(pk[s.lane] < s.pad);
+    const int n = min(max(s.pad - a.t0 - ti.base, 0), kKeyTile);
+    return n >= 64 ? ~0ull : ((1ull << n) - 1);
   };
   auto dma_v = [&](char* dst, const TileInfo& ti) __device__ {
     dma_rows<BF16, D, false>(dst, tile_src(ti, false), ti, s);
@@ -348,16 +379,25 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   float m_run = kNegInf, l_run = 0.0f;
 
   // softmax of tile t (S^T in sacc) and O^T += V^T P^T
-  auto sweep1_tile = [&](auto mask_tag, f32x16* sacc, const char* vs, const TileInfo& ti) __device__ {
+  auto sweep1_tile = [&](auto mask_tag, f32x16* sacc, const char* vs, const TileInfo& ti,
+                         uint64_t padk) __device__ {
     constexpr bool MASK = decltype(mask_tag)::value;
     if constexpr (MASK) {
-      // key k of the tile is visible iff k <= lim_k
+      // key k of the tile is visible iff k <= lim_k and, for a real query row,
+      // the key is no pad token (a pad row keeps its causal keys: its output
+      // and score contributions are dropped later)
       const int lim_k = ti.cache ? ti.valid - 1 : qrow - ti.base;
+      // this lane's keys all have bit 3 equal to h: shift the pad bits once
+      const uint64_t hide = PAD && !s.qpad ? (padk >> (8 * s.h)) : 0;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          sacc[st][r] = st_key(st, r >> 2, r & 3, s.h) <= lim_k ? sacc[st][r] : kNegInf;
+        for (int r = 0; r < 16; ++r) {
+          const int k = st_key(st, r >> 2, r & 3, s.h);
+          const int kb = st_key(st, r >> 2, r & 3, 0);   // compile-time bit of hide
+          const bool vis = k <= lim_k && !(PAD && ((hide >> kb) & 1));
+          sacc[st][r] = vis ? sacc[st][r] : kNegInf;
+        }
     }
     // tile max on the raw logits (the scale is positive), then one fma per exp2
     float tmax = kNegInf;
@@ -371,7 +411,8 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     // 2^kRescaleLog2 (exact in fp32, fine in bf16) and the O rescale is rare.
     if (__ballot(tmax * c2 > m_run + kRescaleLog2) != 0) {
       const float m_new = fmaxf(m_run, tmax * c2);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      // (a padded row that has seen no key yet keeps m = -inf: nothing to scale)
+      const float alpha = PAD && m_new == kNegInf ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
       m_run = m_new;
 #pragma unroll
@@ -380,11 +421,15 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         for (int r = 0; r < 16; ++r) oacc[mt][r] *= alpha;
     }
     float psum = 0.0f;
+    // with left padding a row's first tiles can be all pad keys: m_run is still
+    // -inf there and every logit is -inf, so subtract 0 to get p = 0, not NaN
+    // (without padding every row sees a key in its first tile)
+    const float m_sub = PAD && m_run == kNegInf ? 0.0f : m_run;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][r], c2, -m_run));
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][r], c2, -m_sub));
         sacc[st][r] = p;
         psum += p;
       }
@@ -443,9 +488,9 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   };
 
   // prologue: K(0), V(0), K(1) land in LDS; logits of tile 0
-  dma_k(kb0, tile_info(a, s, 0));
+  dma_k(kb0, tile_info(a, s, 0), 0);
   dma_v(vb0, tile_info(a, s, 0));
-  if (nt > 1) dma_k(kb1, tile_info(a, s, 1));
+  if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   // logits ping-pong between two register sets; the loop is unrolled by two so
@@ -461,18 +506,19 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     char* k_next = P == 0 ? kb1 : kb0;
     char* v_cur = P == 0 ? vb0 : vb1;
     char* v_fill = P == 0 ? vb1 : vb0;
+    const int32_t* pk_cur = pk_ring[t % 3];       // positions of tile t
     const TileInfo ti = tile_info(a, s, t);
-    if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2));
+    if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2), t + 2);
     if (t + 1 < nt) {
       const TileInfo tn = tile_info(a, s, t + 1);
       dma_v(v_fill, tn);
       if (tile_active(s, tn)) qk_st(k_next, nxt);
     }
     if (tile_active(s, ti)) {
-      if (tile_masked(s, ti))
-        sweep1_tile(std::true_type{}, cur, v_cur, ti);
+      if (tile_masked(a, s, ti))
+        sweep1_tile(std::true_type{}, cur, v_cur, ti, pad_bits(ti, pk_cur));
       else
-        sweep1_tile(std::false_type{}, cur, v_cur, ti);
+        sweep1_tile(std::false_type{}, cur, v_cur, ti, 0);
     }
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
@@ -487,7 +533,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   float lse2 = kPosInf;
   if (s.wave_active) {
     const float inv = 1.0f / l_tot;
-    lse2 = s.qvalid ? m_run + __builtin_amdgcn_logf(l_tot) : kPosInf;
+    lse2 = s.qvalid && !s.qpad ? m_run + __builtin_amdgcn_logf(l_tot) : kPosInf;
     if (s.qvalid) {
       const int qh = s.hk * G + s.g;
       E* o = static_cast<E*>(a.o) + (((int64_t)s.bi * a.n_heads + qh) * a.seq_ld + s.row) * D;
@@ -496,8 +542,10 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int d0 = 32 * mt + 8 * i + 4 * s.h;
-          const float x0 = oacc[mt][4 * i + 0] * inv, x1 = oacc[mt][4 * i + 1] * inv;
-          const float x2 = oacc[mt][4 * i + 2] * inv, x3 = oacc[mt][4 * i + 3] * inv;
+          // a pad row has no output (zeros)
+          const float sc = s.qpad ? 0.0f : inv;
+          const float x0 = oacc[mt][4 * i + 0] * sc, x1 = oacc[mt][4 * i + 1] * sc;
+          const float x2 = oacc[mt][4 * i + 2] * sc, x3 = oacc[mt][4 * i + 3] * sc;
           if constexpr (BF16) {
             u32x2 w = {pack_bf16x2(x0, x1), pack_bf16x2(x2, x3)};
             *reinterpret_cast<u32x2*>(o + d0) = w;
@@ -518,7 +566,8 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   for (int r = 0; r < 16; ++r) lse_r[r] = __shfl(lse2, 8 * (r >> 2) + 4 * s.h + (r & 3));
   float* partial = a.partial + ((int64_t)s.u * a.npt_stride + s.pt) * a.cap;
 
-  auto sweep2_tile = [&](auto mask_tag, f32x16* acc, const TileInfo& ti, float (*cs)[kKeyTile]) __device__ {
+  auto sweep2_tile = [&](auto mask_tag, f32x16* acc, const TileInfo& ti, float (*cs)[kKeyTile],
+                         uint64_t padk) __device__ {
     constexpr bool MASK = decltype(mask_tag)::value;
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -535,13 +584,15 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         csum += __builtin_amdgcn_exp2f(x);
       }
       csum = xhalf_sum(csum);
+      // a pad key is visible to no real row (pad rows add nothing: lse = +inf)
+      if (PAD && MASK && ((padk >> key) & 1)) csum = 0.0f;
       if (s.h == 0) cs[s.w][key] = csum;
     }
   };
 
   // prologue: K(0), K(1) land in LDS; logits of tile 0
-  dma_k(kb0, tile_info(a, s, 0));
-  if (nt > 1) dma_k(kb1, tile_info(a, s, 1));
+  dma_k(kb0, tile_info(a, s, 0), 0);
+  if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   if (tile_active(s, tile_info(a, s, 0))) qk_s(kb0, sa);
@@ -552,17 +603,18 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     char* k_fill = P == 0 ? kb0 : kb1;
     char* k_next = P == 0 ? kb1 : kb0;
     float (*cs)[kKeyTile] = P == 0 ? cs0 : cs1;
+    const int32_t* pk_cur = pk_ring[t % 3];
     const TileInfo ti = tile_info(a, s, t);
-    if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2));
+    if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2), t + 2);
     if (t + 1 < nt) {
       const TileInfo tn = tile_info(a, s, t + 1);
       if (tile_active(s, tn)) qk_s(k_next, nxt);
     }
     if (tile_active(s, ti)) {
-      if (tile_masked(s, ti))
-        sweep2_tile(std::true_type{}, cur, ti, cs);
+      if (tile_masked(a, s, ti))
+        sweep2_tile(std::true_type{}, cur, ti, cs, pad_bits(ti, pk_cur));
       else
-        sweep2_tile(std::false_type{}, cur, ti, cs);
+        sweep2_tile(std::false_type{}, cur, ti, cs, 0);
     } else if (s.lane < 32) {
       cs[s.w][s.lane] = 0.0f;
       cs[s.w][32 + s.lane] = 0.0f;
@@ -608,7 +660,10 @@ __global__ void __launch_bounds__(256) score_reduce_kernel(PrefillArgs a, int pt
 template <bool BF16, int D, int G>
 hipError_t launch_t(const PrefillArgs& a, hipStream_t stream) {
   dim3 grid((unsigned)(a.units * a.npt_used));
-  hipLaunchKernelGGL((prefill_attn_kernel<BF16, D, G>), grid, dim3(kThreads), 0, stream, a);
+  if (a.pad)
+    hipLaunchKernelGGL((prefill_attn_kernel<BF16, D, G, true>), grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((prefill_attn_kernel<BF16, D, G, false>), grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -69,6 +69,7 @@ class Workload:
     rule: str = "ave"     # ranking rule of a cut: "ave", "sum" or "recent"
     decode_bound: int = 0  # cache bound during decode (0: kv_max)
     accumulate: bool = True  # score sums during prefill
+    pad_max: int = 0      # left padding: sample j has pads[j] in [0, pad_max] pad tokens
 
     @property
     def group(self) -> int:
@@ -196,6 +197,21 @@ def unit_inputs(wl: Workload, layer: int, sample: int, kv_head: int, sharp: bool
         q = (q * scale).astype(np.float32)
         k = k * key_scale_profile(wl, layer, sample)[:, None]
     return (round_to_dtype(q, wl.dtype), round_to_dtype(k, wl.dtype), round_to_dtype(v, wl.dtype))
+
+
+def sample_pads(wl: Workload) -> np.ndarray:
+    """Left pad tokens per sample (Sec. 3: sample j's prompt is s_j = s - pad_j
+    tokens long): uniform on [0, pad_max], sample 0 unpadded and the last
+    sample padded by exactly pad_max; zeros without padding."""
+    pads = np.zeros(wl.b, dtype=np.int32)
+    if wl.pad_max <= 0:
+        return pads
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([wl.seed, 5])))
+    pads[:] = rng.integers(0, wl.pad_max + 1, size=wl.b)
+    pads[0] = 0
+    if wl.b > 1:
+        pads[-1] = wl.pad_max
+    return pads
 
 
 def checked_units(wl: Workload, count: int, seed: int = 0) -> list:

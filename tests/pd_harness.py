@@ -141,11 +141,15 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
         pd.set_decode_bound(decode_bound)
     if not accumulate:
         pd.set_score_accumulation(False)
+    pads = synth.sample_pads(wl)
+    if wl.pad_max > 0:
+        pd.set_left_padding(torch.from_numpy(pads).to(pd.device))
     sc = accumulate
     G = wl.group
     uin = {u: synth.unit_inputs(wl, 0, u[0], u[1], sharp=sharp) for u in checked}
     orcs = {u: opd.StepOracle(head_dim=wl.head_dim, group=G, kv_max=wl.kv_max,
-                              sm_scale=wl.sm_scale, rule=rule) for u in checked}
+                              sm_scale=wl.sm_scale, rule=rule, pad=int(pads[u[0]]))
+            for u in checked}
     tol = OUT_TOL[wl.dtype]
     D = wl.n_decode if decode_steps is None else decode_steps
 

@@ -296,3 +296,17 @@ def test_decode_cache_lengths_follow_the_oracle(p):
     assert bmx.decode_cache_lengths(s=s, kv_max=kv_max, n_decode=n_decode, p=p) == seen
     # prompt shorter than the bound: the cache first fills during decode
     assert bmx.decode_cache_lengths(s=5, kv_max=8, n_decode=6, p=2) == [5, 6, 7, 6, 7, 6]
+
+
+def test_padded_prefill_flops():
+    # no padding: the plain count; a pad of whole blocks: the unpadded count of
+    # the shorter prompt (pads leave before any real entry, so the real cache
+    # evolves as without them); the count never grows with padding
+    kw = dict(n_kv_heads=2, group=4, head_dim=64, kv_max=96, block=32)
+    assert bmx.prefill_flops_padded(pads=[0, 0, 0], s=300, **kw) == \
+        bmx.prefill_flops(b=3, s=300, **kw)
+    for k in (1, 3, 5):
+        assert bmx.prefill_flops_padded(pads=[32 * k], s=320, **kw) == \
+            bmx.prefill_flops(b=1, s=320 - 32 * k, **kw)
+    f = [bmx.prefill_flops_padded(pads=[p], s=300, **kw) for p in range(0, 300, 7)]
+    assert all(a >= b for a, b in zip(f, f[1:]))

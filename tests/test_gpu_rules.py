@@ -144,3 +144,33 @@ def test_unaccumulated_scores_reject_score_ranked_cut():
     pd.evict_compact(127)
     torch.cuda.synchronize()
     assert sorted(pd.pos[0, 0, :64].tolist()) == list(range(64, 128))
+
+
+# --- left padding (Sec. 3): per-sample prompt lengths s_j = s - pad_j -------------
+@pytest.mark.parametrize("case", [
+    # pads below, across and beyond the first cut; one sample unpadded, one by pad_max
+    dict(dtype="bf16", b=4, n_heads=32, n_kv_heads=8, head_dim=128, s=1024, kv_max=512,
+         block=256, n_decode=16, pad_max=700),
+    dict(dtype="bf16", b=3, n_heads=8, n_kv_heads=4, head_dim=64, s=300, kv_max=100, block=48,
+         n_decode=12, pad_max=250),
+    dict(dtype="f32", b=3, n_heads=8, n_kv_heads=2, head_dim=128, s=200, kv_max=70, block=33,
+         n_decode=7, pad_max=150),
+], ids=lambda c: f"{c['dtype']}-d{c['head_dim']}-s{c['s']}-kv{c['kv_max']}-pad{c['pad_max']}")
+def test_left_padding_all_units(case):
+    wl = C2.with_(name="padded", hh_mode="scatter", n_sinks=4, **case)
+    st = _run(wl, synth.checked_units(wl, wl.units))
+    assert st.cuts > 0
+
+
+def test_left_padding_with_literal_decode_and_long_prompt_pad():
+    # a sample padded for most of the prompt: pads fill whole cache tiles
+    wl = C2.with_(name="padded", b=3, s=2048, kv_max=512, block=256, n_decode=70, pad_max=1900)
+    _run(wl, synth.checked_units(wl, wl.units), decode_p=64)
+
+
+def test_left_padding_full_cache_long_decode():
+    # FKV with padding: K6 masks pad entries too (decode over 4201+ entries)
+    wl = C2.with_(name="padded", b=2, n_heads=8, n_kv_heads=2, s=4200, kv_max=4208, block=256,
+                  n_decode=6, pad_max=3000)
+    st = _run(wl, synth.checked_units(wl, wl.units), accumulate=False)
+    assert st.cuts == 0

@@ -125,3 +125,12 @@ def test_stack_planner():
                                            dtype="bf16")
     assert full == 32 * 8 * 8192 * 128 * 2 * 2
     assert b > 9 * (budget // full)          # the bounded caches hold ~10x the samples
+
+
+def test_sample_pads():
+    wl = synth.WORKLOADS["c2"].with_(pad_max=2048)
+    p = synth.sample_pads(wl)
+    assert p.dtype == np.int32 and p.shape == (wl.b,)
+    assert p[0] == 0 and p[-1] == 2048 and p.min() >= 0 and p.max() <= 2048
+    assert np.array_equal(p, synth.sample_pads(wl))          # seeded
+    assert not synth.sample_pads(synth.WORKLOADS["c2"]).any()  # no padding by default

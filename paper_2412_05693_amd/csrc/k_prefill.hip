@@ -192,11 +192,8 @@ __device__ __forceinline__ TileInfo tile_info(const PrefillArgs& a, const Geo& s
 __device__ __forceinline__ bool tile_active(const Geo& s, const TileInfo& ti) {
   return s.wave_active && (ti.cache || ti.base <= s.wlast);
 }
-__device__ __forceinline__ bool tile_masked(const PrefillArgs& a, const Geo& s,
-                                            const TileInfo& ti) {
-  // left padding: cache tiles may hold pad entries; block tiles below the pad
-  const bool pads = s.pad > 0 && (ti.cache || a.t0 + ti.base < s.pad);
-  return pads || (ti.cache ? ti.valid < kKeyTile : ti.base + kKeyTile - 1 > s.wrow0);
+__device__ __forceinline__ bool tile_masked(const Geo& s, const TileInfo& ti) {
+  return ti.cache ? ti.valid < kKeyTile : ti.base + kKeyTile - 1 > s.wrow0;
 }
 
 // Tiles of K (rows in kappa order) and V are copied into LDS with buffer loads
@@ -379,25 +376,28 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   float m_run = kNegInf, l_run = 0.0f;
 
   // softmax of tile t (S^T in sacc) and O^T += V^T P^T
-  auto sweep1_tile = [&](auto mask_tag, f32x16* sacc, const char* vs, const TileInfo& ti,
-                         uint64_t padk) __device__ {
+  // left padding: a real query row sees no pad key (a pad row keeps its causal
+  // keys; its output and score contributions are dropped later).  The lane's
+  // keys all have bit 3 equal to h, so the pad bits are shifted once.
+  auto hide_pads = [&](f32x16* sacc, uint64_t padk) __device__ {
+    const uint64_t hide = s.qpad ? 0 : (padk >> (8 * s.h));
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if ((hide >> st_key(st, r >> 2, r & 3, 0)) & 1) sacc[st][r] = kNegInf;
+  };
+
+  auto sweep1_tile = [&](auto mask_tag, f32x16* sacc, const char* vs, const TileInfo& ti) __device__ {
     constexpr bool MASK = decltype(mask_tag)::value;
     if constexpr (MASK) {
-      // key k of the tile is visible iff k <= lim_k and, for a real query row,
-      // the key is no pad token (a pad row keeps its causal keys: its output
-      // and score contributions are dropped later)
+      // key k of the tile is visible iff k <= lim_k
       const int lim_k = ti.cache ? ti.valid - 1 : qrow - ti.base;
-      // this lane's keys all have bit 3 equal to h: shift the pad bits once
-      const uint64_t hide = PAD && !s.qpad ? (padk >> (8 * s.h)) : 0;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int k = st_key(st, r >> 2, r & 3, s.h);
-          const int kb = st_key(st, r >> 2, r & 3, 0);   // compile-time bit of hide
-          const bool vis = k <= lim_k && !(PAD && ((hide >> kb) & 1));
-          sacc[st][r] = vis ? sacc[st][r] : kNegInf;
-        }
+        for (int r = 0; r < 16; ++r)
+          sacc[st][r] = st_key(st, r >> 2, r & 3, s.h) <= lim_k ? sacc[st][r] : kNegInf;
     }
     // tile max on the raw logits (the scale is positive), then one fma per exp2
     float tmax = kNegInf;
@@ -515,10 +515,14 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       if (tile_active(s, tn)) qk_st(k_next, nxt);
     }
     if (tile_active(s, ti)) {
-      if (tile_masked(a, s, ti))
-        sweep1_tile(std::true_type{}, cur, v_cur, ti, pad_bits(ti, pk_cur));
+      if constexpr (PAD) {
+        const uint64_t padk = pad_bits(ti, pk_cur);
+        if (padk) hide_pads(cur, padk);
+      }
+      if (tile_masked(s, ti))
+        sweep1_tile(std::true_type{}, cur, v_cur, ti);
       else
-        sweep1_tile(std::false_type{}, cur, v_cur, ti, 0);
+        sweep1_tile(std::false_type{}, cur, v_cur, ti);
     }
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
@@ -566,8 +570,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   for (int r = 0; r < 16; ++r) lse_r[r] = __shfl(lse2, 8 * (r >> 2) + 4 * s.h + (r & 3));
   float* partial = a.partial + ((int64_t)s.u * a.npt_stride + s.pt) * a.cap;
 
-  auto sweep2_tile = [&](auto mask_tag, f32x16* acc, const TileInfo& ti, float (*cs)[kKeyTile],
-                         uint64_t padk) __device__ {
+  auto sweep2_tile = [&](auto mask_tag, f32x16* acc, const TileInfo& ti, float (*cs)[kKeyTile]) __device__ {
     constexpr bool MASK = decltype(mask_tag)::value;
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -584,8 +587,6 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         csum += __builtin_amdgcn_exp2f(x);
       }
       csum = xhalf_sum(csum);
-      // a pad key is visible to no real row (pad rows add nothing: lse = +inf)
-      if (PAD && MASK && ((padk >> key) & 1)) csum = 0.0f;
       if (s.h == 0) cs[s.w][key] = csum;
     }
   };
@@ -611,10 +612,21 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       if (tile_active(s, tn)) qk_s(k_next, nxt);
     }
     if (tile_active(s, ti)) {
-      if (tile_masked(a, s, ti))
-        sweep2_tile(std::true_type{}, cur, ti, cs, pad_bits(ti, pk_cur));
+      if (tile_masked(s, ti))
+        sweep2_tile(std::true_type{}, cur, ti, cs);
       else
-        sweep2_tile(std::false_type{}, cur, ti, cs, 0);
+        sweep2_tile(std::false_type{}, cur, ti, cs);
+      if constexpr (PAD) {
+        // a pad key is visible to no real row (pad rows add nothing: lse = +inf)
+        const uint64_t padk = pad_bits(ti, pk_cur);
+        if (padk && s.h == 0) {
+#pragma unroll
+          for (int st = 0; st < 2; ++st) {
+            const int key = 32 * st + kappa(s.n);
+            if ((padk >> key) & 1) cs[s.w][key] = 0.0f;
+          }
+        }
+      }
     } else if (s.lane < 32) {
       cs[s.w][s.lane] = 0.0f;
       cs[s.w][32 + s.lane] = 0.0f;

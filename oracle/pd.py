@@ -65,6 +65,7 @@ class UnitOracle:
     k: np.ndarray = field(default=None)
     v: np.ndarray = field(default=None)
     score: np.ndarray = field(default=None)
+    last_w: np.ndarray = field(default=None)   # weights of the last processed query
     queries_seen: int = 0
     evicted_score_total: float = 0.0
 
@@ -74,6 +75,7 @@ class UnitOracle:
         self.k = np.zeros((0, d), dtype=np.float64)
         self.v = np.zeros((0, d), dtype=np.float64)
         self.score = np.zeros(0, dtype=np.float64)
+        self.last_w = np.zeros(0, dtype=np.float64)
 
     # -- state ----------------------------------------------------------------
     @property
@@ -91,6 +93,7 @@ class UnitOracle:
         self.k = np.concatenate([self.k, np.asarray(k, dtype=np.float64)])
         self.v = np.concatenate([self.v, np.asarray(v, dtype=np.float64)])
         self.score = np.concatenate([self.score, np.zeros(m)])
+        self.last_w = np.concatenate([self.last_w, np.zeros(m)])
 
     # -- attention + score accumulation ----------------------------------------
     def attend(self, q: np.ndarray, first_pos: int) -> np.ndarray:
@@ -117,6 +120,7 @@ class UnitOracle:
         visible = (self.pos[None, :] <= qpos[:, None]) & (self.pos[None, :] >= self.pad)
         visible &= real_q[:, None]                                     # [m, n]
         out = np.zeros((g_heads, m, d))
+        last = np.zeros(self.n)
         for g in range(g_heads):
             logits = self.sm_scale * (q[g] @ self.k.T)                # [m, n]
             logits = np.where(visible, logits, -np.inf)
@@ -128,6 +132,9 @@ class UnitOracle:
                 p[real_q] = w / w.sum(axis=1, keepdims=True)           # real rows sum to 1
             out[g] = p @ self.v
             self.score = self.score + p.sum(axis=0)
+            last += p[m - 1]
+        # the last query of the call, summed over the group's heads (TOVA's key)
+        self.last_w = last
         self.queries_seen += g_heads * int(real_q.sum())
         return out
 
@@ -147,7 +154,10 @@ class UnitOracle:
         accumulated ``sum_weights`` itself, the cumulative rule that Sec. 3.2
         corrects because it favours early tokens.  ``"recent"``: the position,
         so the most recent pairs stay (the eviction of Algorithm 3, the
-        extreme decoding-only comparator of Sec. 4).
+        extreme decoding-only comparator of Sec. 4).  ``"tova"``: the weights
+        the last processed query gave each entry, summed over the group's
+        heads (TOVA, one of the related policies of Sec. 2: the current query
+        alone decides).
         """
         if self.rule == "ave":
             return self.averages(curr_id)
@@ -155,6 +165,8 @@ class UnitOracle:
             return self.score.copy()
         if self.rule == "recent":
             return self.pos.astype(np.float64)
+        if self.rule == "tova":
+            return self.last_w.copy()
         raise ValueError(f"unknown ranking rule {self.rule!r}")
 
     def evict(self, curr_id: int, kind: str, target: int | None = None) -> EvictionEvent | None:
@@ -194,6 +206,7 @@ class UnitOracle:
         self.k = self.k[idx]
         self.v = self.v[idx]
         self.score = self.score[idx]
+        self.last_w = self.last_w[idx]
 
     # -- schedule steps -----------------------------------------------------------
     def prefill_block(self, t0: int, q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
@@ -242,7 +255,7 @@ class StepOracle(UnitOracle):
 
     def evict(self, curr_id: int, kind: str, target: int | None = None):
         before = (self.pos.copy(), self.k.copy(), self.v.copy(), self.score.copy(),
-                  self.evicted_score_total)
+                  self.evicted_score_total, self.last_w.copy())
         ev = super().evict(curr_id, kind, target)
         self._last = before if ev is not None else None
         self._last_target = self.kv_max if target is None else target
@@ -251,7 +264,7 @@ class StepOracle(UnitOracle):
     def adopt(self, kept_pos) -> None:
         """Replace the result of the last cut by another kept set of the same size.
         Call it right after that cut (before anything is appended)."""
-        pos, k, v, score, evt = self._last
+        pos, k, v, score, evt, last_w = self._last
         kept_pos = np.asarray(sorted(int(p) for p in kept_pos), dtype=np.int64)
         size = getattr(self, "_last_target", None)
         size = self.kv_max if size is None else size
@@ -265,6 +278,7 @@ class StepOracle(UnitOracle):
         mask = np.ones(pos.shape[0], dtype=bool)
         mask[sel] = False
         self.pos, self.k, self.v, self.score = pos[sel], k[sel], v[sel], score[sel]
+        self.last_w = last_w[sel]
         self.evicted_score_total = evt + float(score[mask].sum())
 
 

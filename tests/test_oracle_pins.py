@@ -138,7 +138,7 @@ def pin_selection_bruteforce(cls):
         if trial % 3 == 0:
             score = rng.random(n)
         u = cls(head_dim=2, group=1, kv_max=kv_max, sm_scale=1.0)
-        u.pos, u.score = pos.astype(np.int64), score
+        u.pos, u.score, u.last_w = pos.astype(np.int64), score, np.zeros(n)
         u.k, u.v = np.zeros((n, 2)), np.zeros((n, 2))
         ev = u.evict(curr_id, "prefill")
         ave = score / (curr_id + 1 - pos)
@@ -298,28 +298,31 @@ def pin_rule_keys_bruteforce(cls):
     the three rules disagree."""
     curr_id = 10
     # pos 0 with sum 3 (ave 3/11), pos 9 with sum 1 (ave 1/2), pos 5 with sum 2 (ave 1/3)
-    want = {"ave": [9], "sum": [0], "recent": [9]}
+    # last query's weights: pos 0 0.2, pos 9 0.1, pos 5 0.7
+    want = {"ave": [9], "sum": [0], "recent": [9], "tova": [5]}
     for rule, kept in want.items():
         u = cls(head_dim=2, group=1, kv_max=1, sm_scale=1.0, rule=rule)
         u.pos, u.score = np.array([0, 9, 5], dtype=np.int64), np.array([3.0, 1.0, 2.0])
+        u.last_w = np.array([0.2, 0.1, 0.7])
         u.k, u.v = np.zeros((3, 2)), np.zeros((3, 2))
         ev = u.evict(curr_id, "prefill")
         assert list(ev.kept_pos) == kept, rule
     rng = np.random.default_rng(37)
-    for trial in range(60):
-        rule = ("ave", "sum", "recent")[trial % 3]
+    for trial in range(80):
+        rule = ("ave", "sum", "recent", "tova")[trial % 4]
         n = int(rng.integers(3, 10))
         kv_max = int(rng.integers(1, n))
         pos = rng.choice(np.arange(0, curr_id + 30), size=n, replace=False)
         score = rng.integers(0, 3, size=n).astype(np.float64) / 2.0   # frequent exact ties
+        lw = rng.integers(0, 3, size=n).astype(np.float64) / 4.0
         u = cls(head_dim=2, group=1, kv_max=kv_max, sm_scale=1.0, rule=rule)
-        u.pos, u.score = pos.astype(np.int64), score
+        u.pos, u.score, u.last_w = pos.astype(np.int64), score, lw
         u.k, u.v = np.zeros((n, 2)), np.zeros((n, 2))
         c = int(pos.max())
         ev = u.evict(c, "prefill")
-        key = {"ave": lambda sc, p: sc / (c + 1 - p), "sum": lambda sc, p: sc,
-               "recent": lambda sc, p: float(p)}[rule]
-        rank = {int(p): (key(sc, int(p)), int(p)) for p, sc in zip(pos, score)}
+        key = {"ave": lambda i, p: score[i] / (c + 1 - p), "sum": lambda i, p: score[i],
+               "recent": lambda i, p: float(p), "tova": lambda i, p: lw[i]}[rule]
+        rank = {int(p): (key(i, int(p)), int(p)) for i, p in enumerate(pos)}
         valid = [list(kept) for kept in itertools.combinations(sorted(rank), kv_max)
                  if min(rank[p] for p in kept) > max(rank[p] for p in set(rank) - set(kept))]
         assert len(valid) == 1 and list(ev.kept_pos) == valid[0], rule
@@ -420,10 +423,46 @@ def pin_left_padding_invariants(cls):
     assert abs(total - G * (s + D - pad)) < 1e-9
 
 
+def pin_tova_last_query_weights(cls):
+    """TOVA's key is the last processed query's attention (summed over the
+    group's heads): with nothing removed it equals SDPA's output for that
+    query against one-hot values; with all-zero keys every weight ties, so
+    TOVA keeps exactly the most recent entries, like Algorithm 3's rule."""
+    rng = np.random.default_rng(61)
+    G, s, d = 2, 20, 8
+    q, k, v = _rand_unit(rng, G, s, d)
+    u = cls(head_dim=d, group=G, kv_max=64, sm_scale=0.5, rule="tova")
+    for t0 in range(0, s, 6):
+        t1 = min(s, t0 + 6)
+        u.prefill_block(t0, q[:, t0:t1], k[t0:t1], v[t0:t1])
+        onehot = torch.eye(t1, dtype=torch.float64)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.tensor(q[:, t1 - 1:t1]), torch.tensor(k[:t1])[None].expand(G, t1, d),
+            onehot[None].expand(G, t1, t1), scale=0.5).numpy()[:, 0].sum(axis=0)
+        order = np.argsort(u.pos)
+        np.testing.assert_allclose(u.last_w[order], ref, rtol=0, atol=1e-12)
+    z = np.zeros((s + 4, d))
+    qq = rng.standard_normal((G, s + 4, d))
+    a = opd.run_unit(qq, z, v[:1].repeat(s + 4, 0), s=s, kv_max=5, block=4, n_decode=4,
+                     sm_scale=1.0, rule="recent")
+    u2 = cls(head_dim=d, group=G, kv_max=5, sm_scale=1.0, rule="tova")
+    kept = []
+    for t0 in range(0, s, 4):
+        u2.prefill_block(t0, qq[:, t0:t0 + 4], z[t0:t0 + 4], z[t0:t0 + 4])
+        ev = u2.evict(t0 + 3, "prefill")
+        if ev is not None:
+            kept.append(list(ev.kept_pos))
+    for t in range(4):
+        _, ev = u2.decode_step(s + t, qq[:, s + t], z[s + t], z[s + t])
+        kept.append(list(ev.kept_pos))
+    assert kept == [list(e.kept_pos) for e in a.events]
+
+
 ALL_PINS = [pin_dense_fixed_point, pin_golden, pin_selection_bruteforce,
             pin_conservation_and_lengths, pin_paper_stated_values, pin_permutation_invariance,
             pin_micro_agreement, pin_super_key, pin_rule_keys_bruteforce, pin_alg3_closed_form,
-            pin_left_padding_is_a_shift, pin_left_padding_invariants]
+            pin_left_padding_is_a_shift, pin_left_padding_invariants,
+            pin_tova_last_query_weights]
 
 
 @pytest.mark.parametrize("pin", ALL_PINS, ids=lambda f: f.__name__)
@@ -517,7 +556,7 @@ class _TieNewestFirst(opd.StepOracle):
                                np.sort(self.pos[order[:n_evict]]), self.pos[by], self.score[by],
                                ave[by], float(ave[order[n_evict]] - ave[order[n_evict - 1]]))
         self._last = (self.pos.copy(), self.k.copy(), self.v.copy(), self.score.copy(),
-                      self.evicted_score_total)
+                      self.evicted_score_total, self.last_w.copy())
         self.evicted_score_total += float(self.score[order[:n_evict]].sum())
         self._keep(keep)
         return ev
@@ -570,6 +609,23 @@ class _RecentKeepsOldest(opd.StepOracle):
         return super().ranking_key(curr_id)
 
 
+class _TovaFirstRow(opd.StepOracle):
+    def attend(self, q, first_pos):
+        out = super().attend(q, first_pos)
+        saved = (self.score.copy(), self.queries_seen)
+        q = np.asarray(q)
+        super().attend(q[:, :1], first_pos)          # weights of the call's first row
+        self.score, self.queries_seen = saved
+        return out
+
+
+class _TovaUsesScores(opd.StepOracle):
+    def ranking_key(self, curr_id):
+        if self.rule == "tova":
+            return self.score.copy()
+        return super().ranking_key(curr_id)
+
+
 class _PadKeysVisible(opd.StepOracle):
     def attend(self, q, first_pos):
         saved = self.pad
@@ -595,7 +651,7 @@ class _PadQueriesScore(opd.StepOracle):
 @pytest.mark.parametrize("mutant", [_DenomOffByOne, _NoSelfAttention, _TieNewestFirst,
                                     _FirstHeadOnly, _NoScale, _TransposedValues, _EvictLargest,
                                     _SumRuleUsesAverages, _RecentKeepsOldest, _PadKeysVisible,
-                                    _PadQueriesScore],
+                                    _PadQueriesScore, _TovaFirstRow, _TovaUsesScores],
                          ids=lambda c: c.__name__)
 def test_planted_mistake_is_caught(mutant):
     failures = 0

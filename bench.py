@@ -495,6 +495,9 @@ def main():
                     help="bm: Batch-Max (default); ed: Algorithm 3's extreme decoding-only "
                          "eviction; fkv: full KV cache (the comparators of Sec. 4, run with the "
                          "same kernels at the largest batch their caches allow)")
+    ap.add_argument("--rule", default="ave", choices=["ave", "sum", "tova"],
+                    help="ranking key of Batch-Max's cuts: ave (Sec. 3.2, default), sum (the "
+                         "cumulative rule it corrects) or tova (the last query's weights)")
     ap.add_argument("--pad-max", type=int, default=0,
                     help="single-layer workloads: left-pad sample j by pad_j in [0, N] tokens "
                          "(per-sample prompt lengths s - pad_j, Sec. 3); value counts real tokens")
@@ -516,6 +519,11 @@ def main():
         sys.exit(2)
 
     overrides = {"decode_p": args.decode_p} if args.decode_p else {}
+    if args.rule != "ave":
+        if args.method != "bm":
+            print("bench.py: --rule applies to Batch-Max (--method bm)", file=sys.stderr)
+            sys.exit(2)
+        overrides["rule"] = args.rule
     if args.pad_max:
         if args.config == "c5":
             print("bench.py: --pad-max applies to the single-layer workloads", file=sys.stderr)
@@ -550,6 +558,7 @@ def main():
                    "decode_removal": (f"{wl.decode_p} at once when full" if wl.decode_p
                                       else "one per step"),
                    "left_pad_max": wl.pad_max,
+                   "rank_rule": wl.rule,
                    "method": {"bm": "Batch-Max (Algorithm 1)",
                               "ed": "extreme decoding-only (Algorithm 3)",
                               "fkv": "full KV cache"}[args.method],

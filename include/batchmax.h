@@ -64,8 +64,12 @@ typedef enum bm_dtype { BM_F32 = 0, BM_BF16 = 1 } bm_dtype;
 typedef enum bm_rank_rule {
   BM_RANK_AVE = 0,    /* score / (curr_id + 1 - pos): the method (Sec. 3.2)        */
   BM_RANK_SUM = 1,    /* score alone: the cumulative rule Sec. 3.2 corrects        */
-  BM_RANK_RECENT = 2  /* pos: keep the most recent pairs (Algorithm 3, the
+  BM_RANK_RECENT = 2, /* pos: keep the most recent pairs (Algorithm 3, the
                          extreme decoding-only comparator of Sec. 4)               */
+  BM_RANK_TOVA = 3    /* the weight the last processed query gave each entry,
+                         summed over the group's heads (TOVA, Sec. 2); needs
+                         score accumulation on (its weights come from the same
+                         pass), kept per entry in the workspace                    */
 } bm_rank_rule;
 
 /* Problem statement (Sec. 3 and Algorithm 1): batch b, padded prompt length

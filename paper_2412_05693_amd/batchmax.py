@@ -23,8 +23,9 @@ LIB_PATH = os.path.join(HERE, "libbatchmax.so")
 
 BM_OK, BM_ERR_INVALID_ARG, BM_ERR_UNSUPPORTED, BM_ERR_CAPACITY, BM_ERR_ORDER, BM_ERR_HIP = range(6)
 BM_F32, BM_BF16 = 0, 1
-BM_RANK_AVE, BM_RANK_SUM, BM_RANK_RECENT = 0, 1, 2
-RANK_RULES = {"ave": BM_RANK_AVE, "sum": BM_RANK_SUM, "recent": BM_RANK_RECENT}
+BM_RANK_AVE, BM_RANK_SUM, BM_RANK_RECENT, BM_RANK_TOVA = 0, 1, 2, 3
+RANK_RULES = {"ave": BM_RANK_AVE, "sum": BM_RANK_SUM, "recent": BM_RANK_RECENT,
+              "tova": BM_RANK_TOVA}
 STATUS_NAMES = {0: "BM_OK", 1: "BM_ERR_INVALID_ARG", 2: "BM_ERR_UNSUPPORTED",
                 3: "BM_ERR_CAPACITY", 4: "BM_ERR_ORDER", 5: "BM_ERR_HIP"}
 
@@ -338,7 +339,7 @@ class PDAttention:
         self._set("removal", p)
 
     def set_rank_rule(self, rule) -> None:
-        """"ave" (default, Sec. 3.2), "sum" or "recent" (or a BM_RANK_* value)."""
+        """"ave" (default, Sec. 3.2), "sum", "recent" or "tova" (or a BM_RANK_* value)."""
         self._set("rule", RANK_RULES.get(rule, rule))
 
     def set_decode_bound(self, bound: int) -> None:

@@ -113,6 +113,8 @@ Layout workspace_layout(const bm_dims& d) {
   off = align256(off + units * cap * sizeof(int32_t));
   l.mcount_off = off;
   off = align256(off + units * sizeof(int32_t));
+  l.lastw_off = off;
+  off = align256(off + units * cap * sizeof(float));
   l.total = off;
   return l;
 }
@@ -260,6 +262,8 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   a.units = ctx->units;
   a.accumulate = ctx->accumulate ? 1 : 0;
   a.pad = ctx->pad;
+  a.lastw = ctx->rule == BM_RANK_TOVA ? reinterpret_cast<float*>(work_at(ctx, ctx->lay.lastw_off))
+                                      : nullptr;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
   hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
@@ -303,6 +307,7 @@ int cut_to(bm_ctx* ctx, int target, int32_t curr_id, hipStream_t stream) {
   a.head_dim = ctx->dims.head_dim;
   a.elem_bytes = ctx->elem_bytes;
   a.rule = ctx->rule;
+  a.lastw = reinterpret_cast<float*>(work_at(ctx, ctx->lay.lastw_off));
   hipError_t e = bm::launch_select(a, stream);
   if (e != hipSuccess) return hip_fail(e, "select launch");
   const int n_evict = ctx->len - target;
@@ -331,7 +336,8 @@ BM_EXPORT int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream)
 
 BM_EXPORT int bm_set_rank_rule(bm_ctx* ctx, int32_t rule) {
   if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
-  if (rule != BM_RANK_AVE && rule != BM_RANK_SUM && rule != BM_RANK_RECENT)
+  if (rule != BM_RANK_AVE && rule != BM_RANK_SUM && rule != BM_RANK_RECENT &&
+      rule != BM_RANK_TOVA)
     return fail(BM_ERR_INVALID_ARG, "unknown ranking rule %d", rule);
   ctx->rule = rule;
   return ok();
@@ -470,6 +476,8 @@ BM_EXPORT int bm_decode_step(bm_ctx* ctx, int32_t pos, const void* q, const void
   a.units = ctx->units;
   a.rule = ctx->rule;
   a.pad = ctx->pad;
+  a.lastw = ctx->rule == BM_RANK_TOVA ? reinterpret_cast<float*>(work_at(ctx, ctx->lay.lastw_off))
+                                      : nullptr;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
   const hipError_t e =
       bm::launch_decode(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);

@@ -31,9 +31,13 @@ constexpr int kMaxBlock = 1024;
 //   BM_RANK_AVE:    ave = score / (curr_id + 1 - pos), correctly rounded fp32
 //   BM_RANK_SUM:    score
 //   BM_RANK_RECENT: pos alone (the oldest entry goes first)
-__device__ __forceinline__ uint64_t rank_key(int rule, float score, int pos, int curr_id) {
+//   BM_RANK_TOVA:   last, the last processed query's weight
+__device__ __forceinline__ uint64_t rank_key(int rule, float score, float last, int pos,
+                                             int curr_id) {
   if (rule == BM_RANK_RECENT) return (uint64_t)(uint32_t)pos;
-  const float k = rule == BM_RANK_SUM ? score : score / (float)(curr_id + 1 - pos);
+  const float k = rule == BM_RANK_SUM    ? score
+                  : rule == BM_RANK_TOVA ? last
+                                         : score / (float)(curr_id + 1 - pos);
   return ((uint64_t)__float_as_uint(k) << 32) | (uint32_t)pos;
 }
 
@@ -46,6 +50,7 @@ struct Layout {
   size_t holes_off;     // int32  [U][cap]       evicted slots below kv_max, slot order
   size_t srcs_off;      // int32  [U][cap]       surviving slots at or above kv_max
   size_t mcount_off;    // int32  [U]            number of moves per unit
+  size_t lastw_off;     // float  [U][cap]       last query's weights (TOVA key)
   size_t total;
 };
 
@@ -66,6 +71,7 @@ struct PrefillArgs {
   int n_heads, n_kv_heads, cap, len0, n_tok, t0, npt_used, npt_stride, units;
   int accumulate;     // 0: outputs only (no score sums; new entries get score 0)
   const int32_t* pad; // [b] left pad tokens per sample, or null
+  float* lastw;       // [U, cap] weights of the block's last query, or null
   float scale_log2;   // sm_scale * log2(e)
 };
 
@@ -80,6 +86,7 @@ struct EvictArgs {
   int32_t* mcount;
   int cap, n, kv_max, curr_id, units, head_dim, elem_bytes;
   int rule;           // bm_rank_rule
+  float* lastw;       // [U, cap] last query's weights (moved with the entries), or null
 };
 
 struct DecodeArgs {
@@ -96,6 +103,7 @@ struct DecodeArgs {
   int n_heads, n_kv_heads, cap, len0, kv_max, cur_pos, units;   // kv_max: the decode bound
   int rule;           // bm_rank_rule
   const int32_t* pad; // [b] left pad tokens per sample, or null
+  float* lastw;       // [U, cap] this step's weights are written here, or null
   float scale_log2;
 };
 

@@ -185,7 +185,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
       const float s = sc[j] + ps;
       sc[j] = s;
-      const uint64_t key = rank_key(a.rule, s, pos_s[j], a.cur_pos);
+      const uint64_t key = rank_key(a.rule, s, ps, pos_s[j], a.cur_pos);
       if (key < best) {
         best = key;
         bslot = j;
@@ -305,6 +305,19 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
     if (tid == 0) {
       score[dst] = sc[len0];
       a.pos[(int64_t)u * a.cap + dst] = a.cur_pos;
+    }
+  }
+  if (a.lastw) {
+    // this step's weights, summed over the group's heads: the TOVA key of the
+    // next cut (the new pair's lands in its slot)
+    float* lw = a.lastw + (int64_t)u * a.cap;
+    for (int j = tid; j <= len0; j += 256) {
+      const int slot = j < len0 ? j : dst;
+      if ((j < len0 && j == dst) || slot < 0 || slot >= len0 + (evict ? 0 : 1)) continue;
+      float ps = 0.0f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
+      lw[slot] = ps;
     }
   }
   if (tid == 0) a.len[u] = evict ? len0 : len0 + 1;

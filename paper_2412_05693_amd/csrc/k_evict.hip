@@ -53,6 +53,8 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
   const int tid = threadIdx.x;
   const float* score = a.score + (int64_t)u * a.cap;
   const int32_t* pos = a.pos + (int64_t)u * a.cap;
+  // TOVA's weights (any slot of the unit when the rule does not read them)
+  const float* last = a.rule == BM_RANK_TOVA ? a.lastw + (int64_t)u * a.cap : score;
   const int per = (a.n + 255) / 256;
   constexpr int KP = STREAM ? 1 : kMaxPer;
 
@@ -61,14 +63,14 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
 #pragma unroll
     for (int i = 0; i < kMaxPer; ++i) {
       const int j = tid + 256 * i;
-      key[i] = (i < per && j < a.n) ? rank_key(a.rule, score[j], pos[j], a.curr_id) : ~0ull;
+      key[i] = (i < per && j < a.n) ? rank_key(a.rule, score[j], last[j], pos[j], a.curr_id) : ~0ull;
     }
   }
   // key of entry tid + 256 i (registers, or recomputed when streaming)
   auto key_of = [&](int i) __device__ -> uint64_t {
     if constexpr (STREAM) {
       const int j = tid + 256 * i;
-      return j < a.n ? rank_key(a.rule, score[j], pos[j], a.curr_id) : ~0ull;
+      return j < a.n ? rank_key(a.rule, score[j], last[j], pos[j], a.curr_id) : ~0ull;
     } else {
       return key[i];
     }
@@ -176,6 +178,7 @@ __global__ void __launch_bounds__(256) compact_kernel(EvictArgs a, int nchunks) 
       const int s = srcs[mi], d = holes[mi];
       a.score[(int64_t)u * a.cap + d] = a.score[(int64_t)u * a.cap + s];
       a.pos[(int64_t)u * a.cap + d] = a.pos[(int64_t)u * a.cap + s];
+      if (a.rule == BM_RANK_TOVA) a.lastw[(int64_t)u * a.cap + d] = a.lastw[(int64_t)u * a.cap + s];
     }
   }
 }

@@ -248,6 +248,9 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   // positions of the cached keys of tile t in pk_ring[t % 3] (left padding
   // only): tile t's positions are read while tile t + 2's are being fetched
   __shared__ int32_t pk_ring[3][kKeyTile];
+  // the block's last query's weights per wave (TOVA's key), double-buffered like cs
+  __shared__ float lws0[kWaves][kKeyTile];
+  __shared__ float lws1[kWaves][kKeyTile];
   const Geo s = make_geo<G, PAD>(a);
   const int tid = threadIdx.x;
 
@@ -569,6 +572,18 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 #pragma unroll
   for (int r = 0; r < 16; ++r) lse_r[r] = __shfl(lse2, 8 * (r >> 2) + 4 * s.h + (r & 3));
   float* partial = a.partial + ((int64_t)s.u * a.npt_stride + s.pt) * a.cap;
+  // TOVA: the workgroup holding the block's last row also keeps that row's
+  // weights (summed over the heads) for every key; its waves for that row find
+  // it in accumulator register ri of lane half hr
+  constexpr int PT = kWaves * kRowsPerWave / G;
+  const int last_row = a.n_tok - 1;
+  const bool wg_last = a.lastw && s.pbase <= last_row && last_row < s.pbase + PT;
+  const bool wave_last = wg_last && s.wrow0 <= last_row && last_row < s.wrow0 + kRowsPerWave;
+  const int rl = last_row - s.wrow0;
+  const int ri = 4 * (rl >> 3) + (rl & 3), hr = (rl >> 2) & 1;
+  float lse_last = lse_r[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) lse_last = r == ri ? lse_r[r] : lse_last;
 
   auto sweep2_tile = [&](auto mask_tag, f32x16* acc, const TileInfo& ti, float (*cs)[kKeyTile]) __device__ {
     constexpr bool MASK = decltype(mask_tag)::value;
@@ -604,6 +619,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     char* k_fill = P == 0 ? kb0 : kb1;
     char* k_next = P == 0 ? kb1 : kb0;
     float (*cs)[kKeyTile] = P == 0 ? cs0 : cs1;
+    float (*lws)[kKeyTile] = P == 0 ? lws0 : lws1;
     const int32_t* pk_cur = pk_ring[t % 3];
     const TileInfo ti = tile_info(a, s, t);
     if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2), t + 2);
@@ -631,6 +647,24 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       cs[s.w][s.lane] = 0.0f;
       cs[s.w][32 + s.lane] = 0.0f;
     }
+    if (wg_last) {
+      // the last row sees every key of the tile (pads aside)
+      const uint64_t padk = PAD ? pad_bits(ti, pk_cur) : 0;
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const int key = 32 * st + kappa(s.n);
+        float v = 0.0f;
+        if (wave_last && tile_active(s, ti)) {
+          float z = cur[st][0];
+#pragma unroll
+          for (int r = 1; r < 16; ++r) z = r == ri ? cur[st][r] : z;
+          v = s.h == hr ? __builtin_amdgcn_exp2f(fmaf(z, c2, -lse_last)) : 0.0f;
+          v = xhalf_sum(v);
+          if (PAD && ((padk >> key) & 1)) v = 0.0f;
+        }
+        if (s.h == 0) lws[s.w][key] = v;
+      }
+    }
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
     if (tid < ti.valid) {
@@ -638,6 +672,12 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) acc += cs[w][tid];
       partial[ti.slot0 + tid] = acc;
+      if (wg_last) {
+        float lw = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) lw += lws[w][tid];
+        a.lastw[(int64_t)s.u * a.cap + ti.slot0 + tid] = lw;
+      }
     }
   };
   for (int t = 0; t < nt; t += 2) {

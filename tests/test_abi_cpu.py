@@ -197,9 +197,9 @@ def test_rule_bound_and_accumulation_setters():
     d = dims()
     ctx = _ctx(d, 128, 520)
     try:
-        for r in (bmx.BM_RANK_AVE, bmx.BM_RANK_SUM, bmx.BM_RANK_RECENT):
+        for r in (bmx.BM_RANK_AVE, bmx.BM_RANK_SUM, bmx.BM_RANK_RECENT, bmx.BM_RANK_TOVA):
             bmx.bm_set_rank_rule(ctx, r)
-        assert status_of(bmx.bm_set_rank_rule, ctx, 3) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(bmx.bm_set_rank_rule, ctx, 4) == bmx.BM_ERR_INVALID_ARG
         assert status_of(bmx.bm_set_rank_rule, ctx, -1) == bmx.BM_ERR_INVALID_ARG
         for bnd in (1, 2, d.kv_max):
             bmx.bm_set_decode_bound(ctx, bnd)

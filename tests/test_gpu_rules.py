@@ -174,3 +174,22 @@ def test_left_padding_full_cache_long_decode():
                   n_decode=6, pad_max=3000)
     st = _run(wl, synth.checked_units(wl, wl.units), accumulate=False)
     assert st.cuts == 0
+
+
+# --- TOVA: the last processed query alone ranks the entries -----------------------
+def test_tova_rule_c2_shape():
+    wl = C2.with_(b=2, s=1024, n_decode=24)
+    st = _run(wl, synth.checked_units(wl, wl.units), rule="tova")
+    assert st.cuts == wl.units * (1024 // 256 - 512 // 256 + 24)
+
+
+@pytest.mark.parametrize("case", [
+    dict(dtype="f32", b=2, n_heads=8, n_kv_heads=2, head_dim=128, s=200, kv_max=70, block=33,
+         n_decode=9),
+    dict(dtype="bf16", b=3, n_heads=8, n_kv_heads=4, head_dim=64, s=300, kv_max=100, block=48,
+         n_decode=12, pad_max=250),
+], ids=lambda c: f"{c['dtype']}-d{c['head_dim']}-pad{c.get('pad_max', 0)}")
+def test_tova_rule_ragged_literal_decode(case):
+    # the literal schedule's pre-cut ranks by the previous step's weights
+    wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, **case)
+    _run(wl, synth.checked_units(wl, wl.units), rule="tova", decode_p=4)

@@ -77,6 +77,22 @@ def test_ragged_shapes_all_units(case):
     _run(wl, synth.checked_units(wl, wl.units))
 
 
+@pytest.mark.parametrize("case", [
+    # the smallest bound: every cut keeps one entry
+    dict(dtype="bf16", b=2, n_heads=4, n_kv_heads=4, head_dim=64, s=37, kv_max=1, block=3,
+         n_decode=5),
+    dict(dtype="f32", b=1, n_heads=2, n_kv_heads=1, head_dim=128, s=20, kv_max=1, block=1,
+         n_decode=3),
+    # one sample, one KV head, a prompt shorter than one block
+    dict(dtype="bf16", b=1, n_heads=4, n_kv_heads=1, head_dim=128, s=5, kv_max=3, block=64,
+         n_decode=4),
+], ids=lambda c: f"{c['dtype']}-s{c['s']}-kv{c['kv_max']}-B{c['block']}")
+def test_degenerate_bounds(case):
+    wl = C2.with_(name="degenerate", hh_mode="scatter", n_sinks=0, **case)
+    st = _run(wl, synth.checked_units(wl, wl.units))
+    assert st.cuts > 0
+
+
 def test_no_eviction_dense_fixed_point():
     # bound >= s + D: nothing is ever evicted, every output is dense causal attention
     wl = C2.with_(b=2, s=600, kv_max=700, block=256, n_decode=10)

@@ -220,7 +220,7 @@ def decode_bytes(bmx, wl, b):
     return total
 
 
-def gpu_bench(name, overrides, steps, warmup, method="bm"):
+def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
     import torch
 
     from paper_2412_05693_amd import batchmax as bmx
@@ -255,8 +255,7 @@ def gpu_bench(name, overrides, steps, warmup, method="bm"):
                 ev["ev"][bi_][1].record(stream)
         if ev is not None:
             ev["dec"][0].record(stream)
-        for t in range(wl.n_decode):
-            pd.decode_step(wl.s + t, q, k, v, o, row=wl.s + t)
+        run_decode_loop()
         if ev is not None:
             ev["dec"][1].record(stream)
 
@@ -265,9 +264,22 @@ def gpu_bench(name, overrides, steps, warmup, method="bm"):
         return {"pf": [(mk(), mk()) for _ in blocks], "ev": [(mk(), mk()) for _ in blocks],
                 "dec": (mk(), mk())}
 
+    def run_decode_loop():
+        for t in range(wl.n_decode):
+            pd.decode_step(wl.s + t, q, k, v, o, row=wl.s + t)
+
     for _ in range(warmup):
         one_step()
     torch.cuda.synchronize()
+    if graph and wl.n_decode:
+        # the decode loop as one HIP graph, recorded where the decode starts
+        pd.reset()
+        for (t0, n) in blocks:
+            pd.prefill_block(t0, n, q, k, v, o)
+            pd.evict_compact(t0 + n - 1)
+        dec_graph = pd.capture_decode(q, k, v, o)
+        torch.cuda.synchronize()
+        run_decode_loop = dec_graph.replay
     evs = [new_events() for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -501,6 +513,8 @@ def main():
     ap.add_argument("--pad-max", type=int, default=0,
                     help="single-layer workloads: left-pad sample j by pad_j in [0, N] tokens "
                          "(per-sample prompt lengths s - pad_j, Sec. 3); value counts real tokens")
+    ap.add_argument("--graph", action="store_true",
+                    help="single-layer workloads: replay the decode loop as one HIP graph")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -536,7 +550,8 @@ def main():
         res = gpu_bench_stack(args.config, overrides, args.steps, args.warmup, args.batch,
                               method=args.method)
     else:
-        res = gpu_bench(args.config, overrides, args.steps, args.warmup, method=args.method)
+        res = gpu_bench(args.config, overrides, args.steps, args.warmup, method=args.method,
+                        graph=args.graph)
     wl = res["workload"]
     line = {
         "metric": ("P&D tokens/s (prefill+decode) at max batch; prefill MFMA %, decode HBM GB/s"
@@ -559,6 +574,7 @@ def main():
                                       else "one per step"),
                    "left_pad_max": wl.pad_max,
                    "rank_rule": wl.rule,
+                   "decode_graph": bool(args.graph and args.config != "c5"),
                    "method": {"bm": "Batch-Max (Algorithm 1)",
                               "ed": "extreme decoding-only (Algorithm 3)",
                               "fkv": "full KV cache"}[args.method],

@@ -388,6 +388,25 @@ class PDAttention:
         for t in range(steps):
             self.decode_step(s + t, q, k, v, o, row=r0 + t)
 
+    def capture_decode(self, q, k, v, o, steps=None, first_row=None):
+        """Record run_decode's launches into one HIP graph (the decode loop of
+        Algorithm 1 without host work between steps) and return it.
+
+        Call it where the decode would start (right after the prefill).  Nothing
+        runs during the capture; the context then describes the state after the
+        decode steps.  Every position, length and pointer is fixed inside the
+        graph, so ``graph.replay()`` is valid whenever the device state equals
+        the one at capture time, e.g. after the same prefill has run again.  The
+        decode path enqueues kernels only (no memset nodes)."""
+        t = self.torch
+        g = t.cuda.CUDAGraph()
+        side = t.cuda.Stream(device=self.device)          # default priority
+        side.wait_stream(t.cuda.current_stream(self.device))
+        with t.cuda.graph(g, stream=side):
+            self.run_decode(q, k, v, o, steps, first_row)
+        t.cuda.current_stream(self.device).wait_stream(side)
+        return g
+
     @property
     def length(self) -> int:
         return bm_ctx_len(self.ctx)

@@ -240,3 +240,37 @@ def test_c4_full_shape_sampled_units():
     wl = synth.WORKLOADS["c4"]
     st = _run(wl, synth.checked_units(wl, 6))
     assert st.cuts > 0
+
+
+@pytest.mark.parametrize("decode_p", [0, 8])
+def test_decode_graph_replays_match_eager(decode_p):
+    # the decode loop captured once, replayed three times, each after a fresh
+    # eager prefill: outputs, scores, positions and lengths equal the eager run
+    _need_gpu()
+    from pd_harness import make_pd
+
+    wl = C2.with_(b=2, s=1024, n_decode=24)
+    q, k, v = synth.batch_inputs(wl, "cuda")
+    o = torch.zeros_like(q)
+    pd = make_pd(wl)
+    pd.set_decode_removal(decode_p)
+    pd.run_prefill(q, k, v, o)
+    pd.run_decode(q, k, v, o)
+    torch.cuda.synchronize()
+    ref = (o.clone(), pd.score.clone(), pd.pos.clone(), pd.len.clone())
+
+    pd.reset()
+    pd.run_prefill(q, k, v, o)
+    g = pd.capture_decode(q, k, v, o)
+    for rep in range(3):
+        pd.reset()
+        o.zero_()
+        pd.run_prefill(q, k, v, o)
+        g.replay()
+        torch.cuda.synchronize()
+        _say(f"[graph] replay {rep} decode_p={decode_p}")
+        assert torch.equal(o, ref[0])
+        L = int(ref[3][0, 0])
+        assert torch.equal(pd.len, ref[3])
+        assert torch.equal(pd.pos[..., :L], ref[2][..., :L])
+        assert torch.equal(pd.score[..., :L], ref[1][..., :L])

@@ -163,10 +163,23 @@ def cpu_baseline_line(m, wl):
     tok = wl.b * (wl.s + wl.n_decode) - int(synth.sample_pads(wl).sum())
     what = "(layer, sample, KV head)" if wl.n_layers > 1 else "(sample, KV head)"
     return {"value": tok / t_full, "unit": "tokens/s", "cores": m["cores"], "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{m['done']} {what} units of {wl.name}, full P&D each, float64 numpy, "
                       f"one unit per process and one BLAS thread; {m['unit_s']:.1f} s of oracle "
-                      f"time in {m['wall']:.1f} s wall, scaled to all {total_units} units of "
+                      f"time in {m['wall']:.1f} s wall, scaled (extrapolated: units are "
+                      f"independent and equal in cost) to all {total_units} units of "
                       f"b={wl.b} over {m['cores']} processes"}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 # ---------------------------------------------------------------------------

@@ -131,7 +131,9 @@ def test_sharp_distribution():
 
 
 def test_c2_full_shape_sampled_units():
-    st = _run(C2, synth.checked_units(C2, 12))
+    # 64 of the 512 units (units are independent; the kernels do not depend on
+    # which unit they process)
+    st = _run(C2, synth.checked_units(C2, 64))
     assert st.cuts > 0
 
 
@@ -229,16 +231,18 @@ def test_snapshot_resume_bit_exact():
     assert torch.equal(pd2.score, pd.score) and torch.equal(pd2.pos, pd.pos)
 
 
-def test_c3_full_shape_sampled_units():
+@pytest.mark.parametrize("sample_seed", [0, 1])
+def test_c3_full_shape_sampled_units(sample_seed):
+    # 2 x 16 seeded units (first and last unit in both)
     wl = synth.WORKLOADS["c3"]
-    st = _run(wl, synth.checked_units(wl, 6))
+    st = _run(wl, synth.checked_units(wl, 16, seed=sample_seed))
     assert st.cuts > 0
 
 
 def test_c4_full_shape_sampled_units():
     # decode-heavy: 512 steps with one eviction each per unit
     wl = synth.WORKLOADS["c4"]
-    st = _run(wl, synth.checked_units(wl, 6))
+    st = _run(wl, synth.checked_units(wl, 32))
     assert st.cuts > 0
 
 

@@ -79,7 +79,11 @@ def test_c5_stack_parity_reduced_batch():
 
     wl = synth.WORKLOADS["c5"].with_(b=2)
     L = wl.n_layers
-    checked = [(0, 0, 0), (0, 1, 7), (L // 2, 0, 3), (L // 2, 1, 4), (L - 1, 0, 5), (L - 1, 1, 0)]
+    # 16 (layer, sample, KV head) units over the first, middle and last layers
+    checked = [(0, 0, 0), (0, 1, 7), (0, 0, 2), (0, 1, 5), (1, 0, 1),
+               (L // 2, 0, 3), (L // 2, 1, 4), (L // 2, 0, 6), (L // 2 + 1, 1, 2),
+               (L - 1, 0, 5), (L - 1, 1, 0), (L - 1, 0, 7), (L - 1, 1, 3), (L - 2, 0, 4),
+               (L - 2, 1, 6), (L // 4, 1, 1)]
     _say(f"[stack] {wl.name} b={wl.b} layers={L} s={wl.s} kv={wl.kv_max} B={wl.block} "
          f"D={wl.n_decode} units={checked}")
     st = run_stack_parity(wl, checked)

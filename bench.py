@@ -93,6 +93,48 @@ def hbm_probe():
     print(f"hbm probe: copied {HBM_PROBE_BYTES} bytes three times", flush=True)
 
 
+def peak_probe():
+    """What the box achieves against the published peaks: the device's compute
+    units, a large bf16 GEMM through the vendor BLAS (matrix cores), and a plain
+    device copy (HBM).  Context for the roofline fractions, not a target."""
+    import torch
+
+    dev = torch.device("cuda", 0)
+    props = torch.cuda.get_device_properties(dev)
+    out = {"device": props.name, "compute_units": props.multi_processor_count,
+           "memory_bytes": props.total_memory}
+    n = 8192
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record()
+    for _ in range(reps):
+        torch.matmul(a, b, out=c)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    out["bf16_gemm_tflops"] = 2 * n ** 3 / (ms * 1e-3) / 1e12
+    x = torch.ones(HBM_PROBE_BYTES, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    out["copy_gb_per_s"] = 2 * HBM_PROBE_BYTES / (ms * 1e-3) / 1e9     # read + write
+    out["bf16_gemm_frac_of_peak"] = out["bf16_gemm_tflops"] / (PEAK_BF16_MFMA / 1e12)
+    out["copy_frac_of_peak"] = out["copy_gb_per_s"] / (PEAK_HBM / 1e9)
+    print(json.dumps({"peak_probe": out}), flush=True)
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, one unit per worker process
 # ---------------------------------------------------------------------------
@@ -528,6 +570,8 @@ def main():
                          "(per-sample prompt lengths s - pad_j, Sec. 3); value counts real tokens")
     ap.add_argument("--graph", action="store_true",
                     help="single-layer workloads: replay the decode loop as one HIP graph")
+    ap.add_argument("--peak-probe", action="store_true",
+                    help="only report what this box achieves: bf16 GEMM TFLOP/s, copy GB/s")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="only run the plain copy used to calibrate HBM byte counters")
     args = ap.parse_args()
@@ -538,6 +582,9 @@ def main():
         args.warmup = 1 if stack else 2
     if args.hbm_probe:
         hbm_probe()
+        return
+    if args.peak_probe:
+        peak_probe()
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "

@@ -587,7 +587,7 @@ def main():
         peak_probe()
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
+        print(f"bench.py: measures one GPU only (--gpus {args.gpus} requested); "
               "the path shards with no communication and is not run across GPUs here.",
               file=sys.stderr)
         sys.exit(2)

@@ -51,7 +51,7 @@ extern "C" {
 typedef enum bm_status {
   BM_OK = 0,
   BM_ERR_INVALID_ARG = 1,  /* null pointer, non-positive size, bad divisibility  */
-  BM_ERR_UNSUPPORTED = 2,  /* head_dim, dtype or group size this build lacks     */
+  BM_ERR_UNSUPPORTED = 2,  /* a head_dim, dtype, group size or size not supported */
   BM_ERR_CAPACITY = 3,     /* the call would overflow the cap = kv_max+block slots */
   BM_ERR_ORDER = 4,        /* position or phase out of the schedule's order      */
   BM_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed          */

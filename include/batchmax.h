@@ -158,19 +158,22 @@ int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q, cons
                      const void* v, void* o, int32_t seq_ld, hipStream_t stream);
 
 /* Cut every unit back to kv_max entries (Algorithm 1 removal step; rule of
- * Sec. 3.2): rank entries by ave = score / (curr_id + 1 - pos) ascending, then
- * by pos ascending, remove the first len - kv_max, and fill the holes among
- * slots 0..kv_max-1 with the survivors from slots kv_max..len-1 (K row, V row,
- * score, pos).  curr_id must be the last processed position.  No-op when the
- * cache holds at most kv_max entries. */
+ * Sec. 3.2): rank entries by ave = score / (curr_id + 1 - pos) ascending (or
+ * by the key bm_set_rank_rule chose), then by pos ascending, remove the first
+ * len - kv_max, and fill the holes among slots 0..kv_max-1 with the survivors
+ * from slots kv_max..len-1 (K row, V row, score, pos).  curr_id must be the
+ * last processed position.  No-op when the cache holds at most kv_max
+ * entries. */
 int bm_evict_compact(bm_ctx* ctx, int32_t curr_id, hipStream_t stream);
 
 /* One decode step at position `pos` (Algorithm 1 decode loop with one removal
  * per step): append the step's (k, v), let the G queries attend to all live
  * entries and the new one, add their probabilities to the scores, and, if the
- * cache then holds more than kv_max entries, remove the one with the smallest
- * (ave, pos) with curr_id = pos -- in place: the new entry overwrites the
- * removed slot, or is dropped if it is itself the one removed.
+ * cache then holds more than kv_max entries (the decode bound, see
+ * bm_set_decode_bound), remove the one with the smallest (ave, pos) -- or the
+ * chosen rule's key -- with curr_id = pos, in place: the new entry overwrites
+ * the removed slot, or is dropped if it is itself the one removed.  The
+ * schedule of bm_set_decode_removal can replace this removal.
  *   q, o  point at [b, n_heads, seq_ld, head_dim] row 0 (the step's row)
  *   k, v  point at [b, n_kv_heads, seq_ld, head_dim] row 0
  * Order: prefill finished (pos == s on the first step, then consecutive),

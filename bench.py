@@ -54,6 +54,14 @@ def source_digest() -> str:
     return h.hexdigest()
 
 
+def counters_apply(wl) -> bool:
+    """The committed counter records describe Batch-Max's prefill launches with
+    score sums and no padding (the ranking rule does not change them, except
+    TOVA's extra per-entry writes)."""
+    return wl.accumulate and wl.pad_max == 0 and wl.rule in ("ave", "sum") and \
+        wl.decode_bound == 0
+
+
 def measured_traffic(workload: str, units: int = 0):
     """HBM bytes per prefill launch from a committed counter record
     (`traffic-record:` line under profiles/), or None when there is none for
@@ -375,7 +383,8 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd = kernels[dom]
-    traffic = measured_traffic(wl.name) if dom == "prefill_attention" else None
+    traffic = (measured_traffic(wl.name) if dom == "prefill_attention" and counters_apply(wl)
+               else None)
     roofline = {"bound": kd["bound"], "achieved": round(kd["achieved"], 3), "peak": kd["peak"],
                 "unit": kd["unit"], "frac": round(kd["frac"], 5), "traffic": traffic,
                 "kernel": dom}
@@ -516,7 +525,8 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm"):
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd_ = kernels[dom]
-    traffic = measured_traffic(wl.name, b * Hk) if dom == "prefill_attention" else None
+    traffic = (measured_traffic(wl.name, b * Hk)
+               if dom == "prefill_attention" and counters_apply(wl) else None)
     roofline = {"bound": kd_["bound"], "achieved": round(kd_["achieved"], 3), "peak": kd_["peak"],
                 "unit": kd_["unit"], "frac": round(kd_["frac"], 5), "traffic": traffic,
                 "kernel": dom}

@@ -1,0 +1,77 @@
+"""Host logic of bench.py (no GPU): the comparators' workloads, the byte and
+flop models behind the roofline figures, which counter records apply, the
+CPU-baseline scaling, and the one-GPU guard."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from paper_2412_05693_amd import batchmax as bmx  # noqa: E402
+from paper_2412_05693_amd import synth  # noqa: E402
+
+
+def test_method_workloads():
+    c5 = synth.WORKLOADS["c5"]
+    ed = bench.method_workload(c5, "ed")
+    assert ed.kv_max == c5.s and ed.rule == "recent" and ed.decode_bound == 2
+    assert ed.decode_p == 1 and not ed.accumulate
+    fkv = bench.method_workload(c5, "fkv")
+    assert fkv.kv_max == c5.s + c5.n_decode and not fkv.accumulate and fkv.rule == "ave"
+    assert bench.method_workload(c5, "bm") == c5
+
+
+def test_counter_records_apply_only_to_their_launches():
+    c2 = synth.WORKLOADS["c2"]
+    assert bench.counters_apply(c2)
+    assert bench.counters_apply(c2.with_(rule="sum"))
+    assert not bench.counters_apply(c2.with_(rule="tova"))
+    assert not bench.counters_apply(c2.with_(pad_max=100))
+    for m in ("ed", "fkv"):
+        assert not bench.counters_apply(bench.method_workload(c2, m))
+
+
+def test_decode_bytes_follow_the_schedule():
+    c2 = synth.WORKLOADS["c2"]
+    per = bmx.decode_bytes_per_step(b=c2.b, n_kv_heads=c2.n_kv_heads, group=c2.group,
+                                    head_dim=c2.head_dim, kv_max=c2.kv_max, elem_bytes=2)
+    assert bench.decode_bytes(bmx, c2, c2.b) == per * c2.n_decode
+    # ED: every step reads one cached entry
+    ed = bench.method_workload(c2, "ed")
+    one = bmx.decode_bytes_per_step(b=c2.b, n_kv_heads=c2.n_kv_heads, group=c2.group,
+                                    head_dim=c2.head_dim, kv_max=1, elem_bytes=2)
+    assert bench.decode_bytes(bmx, ed, c2.b) == one * c2.n_decode
+    # FKV past 4097 entries: the outputs-only byte model (no score traffic)
+    fkv = bench.method_workload(c2, "fkv")
+    lens = bmx.decode_cache_lengths(s=fkv.s, kv_max=fkv.kv_max, n_decode=fkv.n_decode)
+    assert lens[0] == c2.s and lens[-1] == c2.s + c2.n_decode - 1
+    want = sum(bmx.decode_bytes_outputs_only(b=c2.b, n_kv_heads=8, group=4, head_dim=128, n=n,
+                                             elem_bytes=2) if n + 1 > bmx.MAX_DECODE_LEN
+               else bmx.decode_bytes_per_step(b=c2.b, n_kv_heads=8, group=4, head_dim=128,
+                                              kv_max=n, elem_bytes=2) for n in lens)
+    assert bench.decode_bytes(bmx, fkv, c2.b) == want
+
+
+def test_cpu_baseline_scaling():
+    wl = synth.WORKLOADS["c2"]
+    m = {"per_unit_s": 0.5, "cores": 8, "done": 16, "unit_s": 8.0, "wall": 1.2}
+    line = bench.cpu_baseline_line(m, wl)
+    t_full = 0.5 * wl.units / 8
+    assert abs(line["value"] - wl.b * (wl.s + wl.n_decode) / t_full) < 1e-6
+    assert line["kind"] == "oracle" and line["cores"] == 8 and line["cpu"]
+    # padded workloads count real tokens only
+    wp = wl.with_(pad_max=1000)
+    lp = bench.cpu_baseline_line(m, wp)
+    real = wp.b * (wp.s + wp.n_decode) - int(synth.sample_pads(wp).sum())
+    assert abs(lp["value"] - real / t_full) < 1e-6
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr

@@ -193,3 +193,20 @@ def test_tova_rule_ragged_literal_decode(case):
     # the literal schedule's pre-cut ranks by the previous step's weights
     wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, **case)
     _run(wl, synth.checked_units(wl, wl.units), rule="tova", decode_p=4)
+
+
+def test_decode_bound_below_prefill_bound_one_removal_per_step():
+    # the first decode step cuts 512 -> 300 at the last processed position (seen
+    # only through the end state, so the sharp inputs keep near-ties away), then
+    # one removal per step keeps 300
+    wl = C2.with_(b=2, s=1024, n_decode=12)
+    st = _run(wl, synth.checked_units(wl, wl.units), sharp=True, decode_bound=300)
+    assert st.cuts == wl.units * (1024 // 256 - 512 // 256 + 12)
+
+
+def test_ed_algorithm_3_with_left_padding():
+    wl = C2.with_(name="padded", hh_mode="scatter", n_sinks=4, b=3, n_heads=8, n_kv_heads=4,
+                  head_dim=64, s=300, kv_max=300, block=48, n_decode=8, pad_max=200)
+    st = _run(wl, synth.checked_units(wl, wl.units), rule="recent", decode_bound=2, decode_p=1,
+              accumulate=False)
+    assert st.cuts == wl.units * wl.n_decode

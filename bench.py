@@ -283,7 +283,14 @@ def decode_bytes(bmx, wl, b):
     return total
 
 
-def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
+def fused_label(dom, fused_cut):
+    """Name of the timed launch pair: with the fused cut a prefill bracket spans
+    the attention kernel and the fold/cut kernel, so its rate is the pair's (and
+    the attention kernel's counter records do not describe it)."""
+    return "prefill_attention+fold_cut" if fused_cut and dom == "prefill_attention" else dom
+
+
+def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cut=False):
     import torch
 
     from paper_2412_05693_amd import batchmax as bmx
@@ -309,11 +316,15 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
         for bi_, (t0, n) in enumerate(blocks):
             if ev is not None:
                 ev["pf"][bi_][0].record(stream)
-            pd.prefill_block(t0, n, q, k, v, o)
+            if fused_cut:      # block and cut in one call: timed together as prefill
+                pd.prefill_block_cut(t0, n, q, k, v, o)
+            else:
+                pd.prefill_block(t0, n, q, k, v, o)
             if ev is not None:
                 ev["pf"][bi_][1].record(stream)
                 ev["ev"][bi_][0].record(stream)
-            pd.evict_compact(t0 + n - 1)
+            if not fused_cut:
+                pd.evict_compact(t0 + n - 1)
             if ev is not None:
                 ev["ev"][bi_][1].record(stream)
         if ev is not None:
@@ -337,9 +348,7 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
     if graph and wl.n_decode:
         # the decode loop as one HIP graph, recorded where the decode starts
         pd.reset()
-        for (t0, n) in blocks:
-            pd.prefill_block(t0, n, q, k, v, o)
-            pd.evict_compact(t0 + n - 1)
+        pd.run_prefill(q, k, v, o, fused_cut=fused_cut)
         dec_graph = pd.capture_decode(q, k, v, o)
         torch.cuda.synchronize()
         run_decode_loop = dec_graph.replay
@@ -383,11 +392,11 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
     }
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd = kernels[dom]
-    traffic = (measured_traffic(wl.name) if dom == "prefill_attention" and counters_apply(wl)
-               else None)
+    traffic = (measured_traffic(wl.name)
+               if dom == "prefill_attention" and counters_apply(wl) and not fused_cut else None)
     roofline = {"bound": kd["bound"], "achieved": round(kd["achieved"], 3), "peak": kd["peak"],
                 "unit": kd["unit"], "frac": round(kd["frac"], 5), "traffic": traffic,
-                "kernel": dom}
+                "kernel": fused_label(dom, fused_cut)}
     prompt_tokens = int(wl.b * wl.s - pads.sum())        # real tokens only (Sec. 3 padding)
     tokens = prompt_tokens + wl.b * wl.n_decode
     return {
@@ -405,7 +414,7 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False):
 STACK_RESERVE = 3 << 30      # device bytes left to the runtime when planning the batch
 
 
-def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm"):
+def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm", fused_cut=False):
     """The layer stack at the largest batch that fits: per (layer, block) the
     device generator writes the block's Q/K/V, then prefill and the cut; then
     the decode steps, layer by layer.  Generator time is measured and left out
@@ -476,8 +485,11 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm"):
             for layer in range(L):
                 pd = stack.layers[layer]
                 rec("gen", lambda: bmx.synth_qkv(params[layer], t0, q, k, v))
-                rec("pf", lambda: pd.prefill_block(t0, n, q, k, v, o, row=0))
-                rec("cut", lambda: pd.evict_compact(t0 + n - 1))
+                if fused_cut:   # block and cut in one call: timed together as prefill
+                    rec("pf", lambda: pd.prefill_block_cut(t0, n, q, k, v, o, row=0))
+                else:
+                    rec("pf", lambda: pd.prefill_block(t0, n, q, k, v, o, row=0))
+                    rec("cut", lambda: pd.evict_compact(t0 + n - 1))
         for t in range(wl.n_decode):
             p = wl.s + t
             for layer in range(L):
@@ -526,10 +538,10 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm"):
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd_ = kernels[dom]
     traffic = (measured_traffic(wl.name, b * Hk)
-               if dom == "prefill_attention" and counters_apply(wl) else None)
+               if dom == "prefill_attention" and counters_apply(wl) and not fused_cut else None)
     roofline = {"bound": kd_["bound"], "achieved": round(kd_["achieved"], 3), "peak": kd_["peak"],
                 "unit": kd_["unit"], "frac": round(kd_["frac"], 5), "traffic": traffic,
-                "kernel": dom}
+                "kernel": fused_label(dom, fused_cut)}
     if traffic is not None:
         roofline["traffic_basis"] = ("FETCH_SIZE/WRITE_SIZE per unit of the same launches "
                                      "measured on c2, scaled to this launch's units")
@@ -578,6 +590,9 @@ def main():
     ap.add_argument("--pad-max", type=int, default=0,
                     help="single-layer workloads: left-pad sample j by pad_j in [0, N] tokens "
                          "(per-sample prompt lengths s - pad_j, Sec. 3); value counts real tokens")
+    ap.add_argument("--fused-cut", action="store_true",
+                    help="run each prefill block and its cut as one call (fold, select and "
+                         "compaction in one kernel); prefill timings then include the cut")
     ap.add_argument("--graph", action="store_true",
                     help="single-layer workloads: replay the decode loop as one HIP graph")
     ap.add_argument("--peak-probe", action="store_true",
@@ -618,10 +633,10 @@ def main():
         cpu = cpu_baseline(args.config, overrides, args.cpu_seconds, args.method)
     if args.config == "c5":
         res = gpu_bench_stack(args.config, overrides, args.steps, args.warmup, args.batch,
-                              method=args.method)
+                              method=args.method, fused_cut=args.fused_cut)
     else:
         res = gpu_bench(args.config, overrides, args.steps, args.warmup, method=args.method,
-                        graph=args.graph)
+                        graph=args.graph, fused_cut=args.fused_cut)
     wl = res["workload"]
     line = {
         "metric": ("P&D tokens/s (prefill+decode) at max batch; prefill MFMA %, decode HBM GB/s"
@@ -645,6 +660,7 @@ def main():
                    "left_pad_max": wl.pad_max,
                    "rank_rule": wl.rule,
                    "decode_graph": bool(args.graph and args.config != "c5"),
+                   "fused_cut": bool(args.fused_cut),
                    "method": {"bm": "Batch-Max (Algorithm 1)",
                               "ed": "extreme decoding-only (Algorithm 3)",
                               "fkv": "full KV cache"}[args.method],

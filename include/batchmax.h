@@ -157,6 +157,16 @@ int bm_resume(const bm_dims* dims, const bm_cache* cache, int32_t len, int32_t n
 int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q, const void* k,
                      const void* v, void* o, int32_t seq_ld, hipStream_t stream);
 
+/* bm_prefill_block followed by bm_evict_compact(ctx, t0 + n_tok - 1): one
+ * prefill block and its cut (Algorithm 1's step for the block), with the fold
+ * of the block's score sums, the select and the compaction in one kernel (one
+ * workgroup per unit) instead of three launches when the cache then holds at
+ * most 4096 entries; beyond that the separate kernels run.  Same results,
+ * checks and errors as the two calls (a cut that would rank by scores a block
+ * did not add to returns BM_ERR_ORDER before anything is enqueued). */
+int bm_prefill_block_cut(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q, const void* k,
+                         const void* v, void* o, int32_t seq_ld, hipStream_t stream);
+
 /* Cut every unit back to kv_max entries (Algorithm 1 removal step; rule of
  * Sec. 3.2): rank entries by ave = score / (curr_id + 1 - pos) ascending (or
  * by the key bm_set_rank_rule chose), then by pos ascending, remove the first

@@ -79,6 +79,7 @@ def _load() -> ctypes.CDLL:
         "bm_init": (ctypes.c_int, [dims_p, cache_p, P, ctypes.POINTER(P)]),
         "bm_resume": (ctypes.c_int, [dims_p, cache_p, I32, I32, ctypes.POINTER(P)]),
         "bm_prefill_block": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
+        "bm_prefill_block_cut": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
         "bm_evict_compact": (ctypes.c_int, [P, I32, P]),
         "bm_set_decode_removal": (ctypes.c_int, [P, I32]),
         "bm_set_rank_rule": (ctypes.c_int, [P, I32]),
@@ -101,7 +102,8 @@ def _load() -> ctypes.CDLL:
 
 _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
-            "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block", "bm_evict_compact",
+            "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block",
+            "bm_prefill_block_cut", "bm_evict_compact",
             "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
             "bm_set_score_accumulation", "bm_set_left_padding",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
@@ -152,6 +154,11 @@ def bm_resume(dims: bm_dims, cache: bm_cache, length: int, next_pos: int) -> int
 def bm_prefill_block(ctx: int, t0: int, n_tok: int, q: int, k: int, v: int, o: int,
                      seq_ld: int, stream: int) -> None:
     _check(_lib.bm_prefill_block(ctx, t0, n_tok, q, k, v, o, seq_ld, stream))
+
+
+def bm_prefill_block_cut(ctx: int, t0: int, n_tok: int, q: int, k: int, v: int, o: int,
+                         seq_ld: int, stream: int) -> None:
+    _check(_lib.bm_prefill_block_cut(ctx, t0, n_tok, q, k, v, o, seq_ld, stream))
 
 
 def bm_evict_compact(ctx: int, curr_id: int, stream: int) -> None:
@@ -316,7 +323,7 @@ class PDAttention:
         self.ctx = bm_resume(self.dims, self.cache, length, next_pos)
         self._apply_settings()
 
-    def prefill_block(self, t0, n_tok, q, k, v, o, row=None) -> None:
+    def _block_args(self, t0, n_tok, q, k, v, o, row):
         row = t0 if row is None else row
         H, Hk = self.dims.n_heads, self.dims.n_kv_heads
         for x, hh, nm in ((q, H, "q"), (k, Hk, "k"), (v, Hk, "v"), (o, H, "o")):
@@ -326,8 +333,15 @@ class PDAttention:
         T = q.shape[2]
         if not (k.shape[2] == v.shape[2] == o.shape[2] == T):
             raise ValueError("q, k, v and o need the same number of rows")
-        bm_prefill_block(self.ctx, t0, n_tok, self._row_ptr(q, row), self._row_ptr(k, row),
-                         self._row_ptr(v, row), self._row_ptr(o, row), T, self._stream())
+        return (self.ctx, t0, n_tok, self._row_ptr(q, row), self._row_ptr(k, row),
+                self._row_ptr(v, row), self._row_ptr(o, row), T, self._stream())
+
+    def prefill_block(self, t0, n_tok, q, k, v, o, row=None) -> None:
+        bm_prefill_block(*self._block_args(t0, n_tok, q, k, v, o, row))
+
+    def prefill_block_cut(self, t0, n_tok, q, k, v, o, row=None) -> None:
+        """prefill_block then evict_compact(t0 + n_tok - 1), fused where possible."""
+        bm_prefill_block_cut(*self._block_args(t0, n_tok, q, k, v, o, row))
 
     def evict_compact(self, curr_id) -> None:
         bm_evict_compact(self.ctx, curr_id, self._stream())
@@ -372,13 +386,17 @@ class PDAttention:
         bm_decode_step(self.ctx, pos, self._row_ptr(q, row), self._row_ptr(k, row),
                        self._row_ptr(v, row), self._row_ptr(o, row), T, self._stream())
 
-    def run_prefill(self, q, k, v, o) -> None:
-        """Algorithm 1 prefill under the block loop: every block, then a cut."""
+    def run_prefill(self, q, k, v, o, fused_cut=False) -> None:
+        """Algorithm 1 prefill under the block loop: every block, then a cut
+        (with ``fused_cut`` through prefill_block_cut)."""
         s, B = self.dims.s, self.dims.block
         for t0 in range(0, s, B):
             n = min(B, s - t0)
-            self.prefill_block(t0, n, q, k, v, o)
-            self.evict_compact(t0 + n - 1)
+            if fused_cut:
+                self.prefill_block_cut(t0, n, q, k, v, o)
+            else:
+                self.prefill_block(t0, n, q, k, v, o)
+                self.evict_compact(t0 + n - 1)
 
     def run_decode(self, q, k, v, o, steps=None, first_row=None) -> None:
         """Decode steps at positions s, s+1, ... using rows first_row.. (default s)."""

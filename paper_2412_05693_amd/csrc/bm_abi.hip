@@ -217,9 +217,14 @@ BM_EXPORT int bm_resume(const bm_dims* dims, const bm_cache* cache, int32_t len,
   return ok();
 }
 
-BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q,
-                               const void* k, const void* v, void* o, int32_t seq_ld,
-                               hipStream_t stream) {
+namespace {
+
+int check_rule(const bm_ctx* ctx);
+int cut_to(bm_ctx* ctx, int target, int32_t curr_id, hipStream_t stream);
+
+// Checks of a prefill block (all on the host); fills the kernel arguments.
+int prefill_args(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q, const void* k,
+                 const void* v, void* o, int32_t seq_ld, bm::PrefillArgs* out) {
   if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
   if (!q || !k || !v || !o) return fail(BM_ERR_INVALID_ARG, "q, k, v or o is null");
   if (n_tok < 1 || n_tok > ctx->dims.block)
@@ -238,7 +243,7 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   if (ctx->len + n_tok > ctx->cap)
     return fail(BM_ERR_CAPACITY, "len %d + n_tok %d exceeds cap %d", ctx->len, n_tok, ctx->cap);
 
-  bm::PrefillArgs a;
+  bm::PrefillArgs& a = *out;
   a.q = q;
   a.kin = k;
   a.vin = v;
@@ -265,14 +270,78 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   a.lastw = ctx->rule == BM_RANK_TOVA ? reinterpret_cast<float*>(work_at(ctx, ctx->lay.lastw_off))
                                       : nullptr;
   a.scale_log2 = ctx->sm_scale * 1.4426950408889634f;
-  hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
-  if (e != hipSuccess) return hip_fail(e, "prefill launch");
-  e = bm::launch_score_reduce(a, stream);
-  if (e != hipSuccess) return hip_fail(e, "score reduce launch");
+  return BM_OK;
+}
+
+void advance(bm_ctx* ctx, int32_t t0, int32_t n_tok) {
   ctx->len += n_tok;
   ctx->next_pos = t0 + n_tok;
   ctx->last_pos = t0 + n_tok - 1;
   if (!ctx->accumulate) ctx->scores_valid = false;
+}
+
+}  // namespace
+
+BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q,
+                               const void* k, const void* v, void* o, int32_t seq_ld,
+                               hipStream_t stream) {
+  bm::PrefillArgs a;
+  const int st = prefill_args(ctx, t0, n_tok, q, k, v, o, seq_ld, &a);
+  if (st != BM_OK) return st;
+  hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  e = bm::launch_score_reduce(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "score reduce launch");
+  advance(ctx, t0, n_tok);
+  return ok();
+}
+
+BM_EXPORT int bm_prefill_block_cut(bm_ctx* ctx, int32_t t0, int32_t n_tok, const void* q,
+                                   const void* k, const void* v, void* o, int32_t seq_ld,
+                                   hipStream_t stream) {
+  bm::PrefillArgs a;
+  int st = prefill_args(ctx, t0, n_tok, q, k, v, o, seq_ld, &a);
+  if (st != BM_OK) return st;
+  const int n = ctx->len + n_tok;
+  const bool cuts = n > ctx->dims.kv_max;
+  if (cuts && (!ctx->scores_valid || !ctx->accumulate) && ctx->rule != BM_RANK_RECENT)
+    return fail(BM_ERR_ORDER,
+                "a block ran without score accumulation: only BM_RANK_RECENT can rank this cache");
+  hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  if (n > bm::kMaxCap) {
+    // too many entries for the one-workgroup cut: fold, then the two-kernel cut
+    e = bm::launch_score_reduce(a, stream);
+    if (e != hipSuccess) return hip_fail(e, "score reduce launch");
+    advance(ctx, t0, n_tok);
+    if (cuts) {
+      st = cut_to(ctx, ctx->dims.kv_max, ctx->last_pos, stream);
+      if (st != BM_OK) return st;
+    }
+    return ok();
+  }
+  bm::EvictArgs c;
+  c.kc = ctx->cache.k;
+  c.vc = ctx->cache.v;
+  c.score = ctx->cache.score;
+  c.pos = ctx->cache.pos;
+  c.len = ctx->cache.len;
+  c.holes = nullptr;
+  c.srcs = nullptr;
+  c.mcount = nullptr;
+  c.cap = ctx->cap;
+  c.n = n;
+  c.kv_max = ctx->dims.kv_max;
+  c.curr_id = t0 + n_tok - 1;
+  c.units = ctx->units;
+  c.head_dim = ctx->dims.head_dim;
+  c.elem_bytes = ctx->elem_bytes;
+  c.rule = ctx->rule;
+  c.lastw = reinterpret_cast<float*>(work_at(ctx, ctx->lay.lastw_off));
+  e = bm::launch_fold_cut(a, c, bm::positions_per_wg(ctx->group), stream);
+  if (e != hipSuccess) return hip_fail(e, "fold-cut launch");
+  advance(ctx, t0, n_tok);
+  if (cuts) ctx->len = ctx->dims.kv_max;
   return ok();
 }
 

@@ -138,6 +138,8 @@ hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int gro
                           hipStream_t stream);
 hipError_t launch_score_reduce(const PrefillArgs& a, hipStream_t stream);
 hipError_t launch_select(const EvictArgs& a, hipStream_t stream);
+hipError_t launch_fold_cut(const PrefillArgs& pa, const EvictArgs& a, int pt_positions,
+                           hipStream_t stream);
 hipError_t launch_compact(const EvictArgs& a, int max_moves, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group,
                          hipStream_t stream);

@@ -43,6 +43,57 @@ __device__ __forceinline__ int block_excl_count(bool flag, int* s_wave, int* tot
   return before + in_wave;
 }
 
+// The need-th smallest (1-based) of the keys key_of(i) of the entries
+// tid + 256 i < n: an 8-pass radix select over 8-bit digits (histograms in LDS,
+// a 64-lane scan of the 256 bins).  Keys are unique (they hold the position),
+// so exactly `need` keys are <= the result.
+template <typename KeyOf>
+__device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per, int n, int need,
+                                              uint32_t* hist, uint64_t* s_prefix, int* s_need) {
+  const int tid = threadIdx.x;
+  uint64_t prefix = 0;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    const uint64_t himask = pass == 0 ? 0ull : (~0ull << (shift + 8));
+    hist[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < n_iter; ++i) {
+      const int j = tid + 256 * i;
+      if (i < per && j < n) {
+        const uint64_t kk = key_of(i);
+        if ((kk & himask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
+                     h3 = hist[4 * tid + 3];
+      const uint32_t mine = h0 + h1 + h2 + h3;
+      uint32_t incl = mine;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = __shfl_up(incl, off);
+        if (tid >= off) incl += o;
+      }
+      uint32_t ex = incl - mine;
+      const uint32_t hv[4] = {h0, h1, h2, h3};
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        if ((int)ex < need && need <= (int)(ex + hv[b])) {
+          *s_prefix = prefix | ((uint64_t)(4 * tid + b) << shift);
+          *s_need = need - (int)ex;
+        }
+        ex += hv[b];
+      }
+    }
+    __syncthreads();
+    prefix = *s_prefix;
+    need = *s_need;
+  }
+  return prefix;
+}
+
 template <bool STREAM>
 __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
   __shared__ uint32_t hist[256];
@@ -76,50 +127,8 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
     }
   };
   const int n_iter = STREAM ? per : kMaxPer;
-
-  // radix select of the E-th smallest key (1-based)
-  uint64_t prefix = 0;
-  int need = a.n - a.kv_max;
-  for (int pass = 0; pass < 8; ++pass) {
-    const int shift = 56 - 8 * pass;
-    const uint64_t himask = pass == 0 ? 0ull : (~0ull << (shift + 8));
-    hist[tid] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < n_iter; ++i) {
-      const int j = tid + 256 * i;
-      if (i < per && j < a.n) {
-        const uint64_t kk = key_of(i);
-        if ((kk & himask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
-      }
-    }
-    __syncthreads();
-    if (tid < 64) {
-      const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
-                     h3 = hist[4 * tid + 3];
-      const uint32_t mine = h0 + h1 + h2 + h3;
-      uint32_t incl = mine;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t o = __shfl_up(incl, off);
-        if (tid >= off) incl += o;
-      }
-      uint32_t ex = incl - mine;
-      const uint32_t hv[4] = {h0, h1, h2, h3};
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        if ((int)ex < need && need <= (int)(ex + hv[b])) {
-          s_prefix = prefix | ((uint64_t)(4 * tid + b) << shift);
-          s_need = need - (int)ex;
-        }
-        ex += hv[b];
-      }
-    }
-    __syncthreads();
-    prefix = s_prefix;
-    need = s_need;
-  }
-  const uint64_t thr = prefix;  // exactly n - kv_max keys are <= thr
+  const uint64_t thr = radix_kth(key_of, n_iter, per, a.n, a.n - a.kv_max, hist, &s_prefix,
+                                 &s_need);   // exactly n - kv_max keys are <= thr
 
   // holes (evicted, slot < kv_max) and sources (kept, slot >= kv_max), slot order
   int32_t* holes = a.holes + (int64_t)u * a.cap;
@@ -183,7 +192,117 @@ __global__ void __launch_bounds__(256) compact_kernel(EvictArgs a, int nchunks) 
   }
 }
 
+// K7: the fold of K1's partial column sums, the cut and the compaction of one
+// unit in one workgroup (the block's Algorithm 1 step in one launch instead of
+// three).  The folded scores, the positions and TOVA's weights stay in LDS, the
+// keys in registers; the hole and source lists are built in LDS; the moves copy
+// K and V rows with 16-byte loads and stores.  Needs n <= kMaxCap.
+__global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs a,
+                                                        int pt_positions) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint64_t s_prefix;
+  __shared__ int s_need;
+  __shared__ int s_wave[4];
+  // per-slot LDS arrays, n4 = n rounded up to 4 entries each (dynamic size)
+  extern __shared__ __attribute__((aligned(16))) char k7_lds[];
+  const int n = a.n;
+  const int n4 = (n + 3) & ~3;
+  float* sc = reinterpret_cast<float*>(k7_lds);
+  int32_t* ps = reinterpret_cast<int32_t*>(sc + n4);
+  float* lw = reinterpret_cast<float*>(ps + n4);
+  int32_t* holes = reinterpret_cast<int32_t*>(lw + n4);
+  int32_t* srcs = holes + n4;
+  const int u = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int per = (n + 255) / 256;
+  float* score = a.score + (int64_t)u * a.cap;
+  int32_t* pos = a.pos + (int64_t)u * a.cap;
+  float* last = a.rule == BM_RANK_TOVA ? a.lastw + (int64_t)u * a.cap : nullptr;
+  const float* part = pa.partial + (int64_t)u * pa.npt_stride * pa.cap;
+
+  // 1. fold the partial sums (workgroup order, as score_reduce_kernel) and key
+  uint64_t key[kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int j = tid + 256 * i;
+    key[i] = ~0ull;
+    if (i < per && j < n) {
+      const int pt0 = j < pa.len0 ? 0 : (j - pa.len0) / pt_positions;
+      float acc = j < pa.len0 ? score[j] : 0.0f;
+      if (pa.accumulate) {
+#pragma unroll 8
+        for (int pt = pt0; pt < pa.npt_used; ++pt) acc += part[(int64_t)pt * pa.cap + j];
+      }
+      const int p = pos[j];
+      const float l = last ? last[j] : 0.0f;
+      score[j] = acc;
+      sc[j] = acc;
+      ps[j] = p;
+      lw[j] = l;
+      key[i] = rank_key(a.rule, acc, l, p, a.curr_id);
+    }
+  }
+  if (n <= a.kv_max) {
+    if (tid == 0) a.len[u] = n;
+    return;
+  }
+
+  // 2. the cut: the (n - kv_max)-th smallest key, then holes and sources
+  auto key_of = [&](int i) __device__ -> uint64_t { return key[i]; };
+  const uint64_t thr = radix_kth(key_of, kMaxPer, per, n, n - a.kv_max, hist, &s_prefix, &s_need);
+  int hbase = 0, sbase = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    if (i >= per) break;  // uniform across the workgroup
+    const int j = tid + 256 * i;
+    const bool live = j < n;
+    const bool ev = live && key[i] <= thr;
+    const bool is_hole = live && j < a.kv_max && ev;
+    const bool is_src = live && j >= a.kv_max && !ev;
+    int ht, stot;
+    const int hr = block_excl_count(is_hole, s_wave, &ht);
+    const int sr = block_excl_count(is_src, s_wave, &stot);
+    if (is_hole) holes[hbase + hr] = j;
+    if (is_src) srcs[sbase + sr] = j;
+    hbase += ht;
+    sbase += stot;
+  }
+  __syncthreads();
+
+  // 3. the moves: the i-th source into the i-th hole (disjoint slot ranges)
+  const int m = min(hbase, sbase);
+  const int row_bytes = a.head_dim * a.elem_bytes;
+  const int cpr = row_bytes / 16;
+  char* kc = static_cast<char*>(a.kc) + (int64_t)u * a.cap * row_bytes;
+  char* vc = static_cast<char*>(a.vc) + (int64_t)u * a.cap * row_bytes;
+  for (int c = tid; c < m * 2 * cpr; c += 256) {
+    const int mv = c / (2 * cpr);
+    const int rem = c - mv * 2 * cpr;
+    const int which = rem / cpr, cc = rem - which * cpr;
+    char* base = which ? vc : kc;
+    const int64_t src = (int64_t)srcs[mv] * row_bytes + cc * 16;
+    const int64_t dst = (int64_t)holes[mv] * row_bytes + cc * 16;
+    *reinterpret_cast<uint4*>(base + dst) = *reinterpret_cast<const uint4*>(base + src);
+  }
+  for (int mv = tid; mv < m; mv += 256) {
+    const int sj = srcs[mv], dj = holes[mv];
+    score[dj] = sc[sj];
+    pos[dj] = ps[sj];
+    if (last) last[dj] = lw[sj];
+  }
+  if (tid == 0) a.len[u] = a.kv_max;
+}
+
 }  // namespace
+
+hipError_t launch_fold_cut(const PrefillArgs& pa, const EvictArgs& a, int pt_positions,
+                           hipStream_t stream) {
+  if (a.n > kMaxCap) return hipErrorInvalidValue;
+  const size_t lds = 5 * sizeof(int32_t) * (size_t)((a.n + 3) & ~3);
+  hipLaunchKernelGGL(fold_cut_kernel, dim3((unsigned)a.units), dim3(256), lds, stream, pa, a,
+                     pt_positions);
+  return hipGetLastError();
+}
 
 hipError_t launch_select(const EvictArgs& a, hipStream_t stream) {
   if (a.n > kMaxCap)

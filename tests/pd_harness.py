@@ -117,7 +117,7 @@ def _compare_cut(tag, orc: opd.StepOracle, ev, gpu_pos, st: Stats):
 
 def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decode_steps=None,
                inputs=None, pd=None, stop_on_failure=True, decode_p=0, rule="ave",
-               decode_bound=None, accumulate=True) -> Stats:
+               decode_bound=None, accumulate=True, fused_cut=False) -> Stats:
     """Run the whole P&D schedule on the device and compare the checked units.
 
     ``decode_p > 0`` selects Algorithm 1's decoding loop taken literally (a step
@@ -125,7 +125,9 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
     is compared against the device's live set without the step's new entry.
     ``rule`` is the ranking rule of every cut, ``decode_bound`` the cache bound
     during decode (default kv_max).  ``accumulate=False`` runs the prefill
-    without score sums: scores are then not compared (only positions)."""
+    without score sums: scores are then not compared (only positions).
+    ``fused_cut`` runs each block and its cut as one call (the state between
+    the two is then not observed)."""
     st = Stats()
     if inputs is None:
         inputs = synth.batch_inputs(wl, device, checked=checked, sharp=sharp)
@@ -163,16 +165,23 @@ def run_parity(wl: synth.Workload, checked, *, sharp=False, device="cuda", decod
 
     for t0 in range(0, wl.s, wl.block):
         n = min(wl.block, wl.s - t0)
-        pd.prefill_block(t0, n, q, k, v, o)
-        length = pd.length
-        pos, score, dlen = _snapshot(pd, checked, length)
-        for i, u in enumerate(checked):
-            uq, uk, uv = uin[u]
-            ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
-            check_out(f"block {t0}", u, slice(t0, t0 + n), ref)
-            _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i], length, st,
-                           sc)
-        pd.evict_compact(t0 + n - 1)
+        if fused_cut:
+            pd.prefill_block_cut(t0, n, q, k, v, o)
+            for u in checked:
+                uq, uk, uv = uin[u]
+                ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
+                check_out(f"block {t0}", u, slice(t0, t0 + n), ref)
+        else:
+            pd.prefill_block(t0, n, q, k, v, o)
+            length = pd.length
+            pos, score, dlen = _snapshot(pd, checked, length)
+            for i, u in enumerate(checked):
+                uq, uk, uv = uin[u]
+                ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
+                check_out(f"block {t0}", u, slice(t0, t0 + n), ref)
+                _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i], length,
+                               st, sc)
+            pd.evict_compact(t0 + n - 1)
         length = pd.length
         pos, score, dlen = _snapshot(pd, checked, length)
         for i, u in enumerate(checked):

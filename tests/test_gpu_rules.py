@@ -210,3 +210,25 @@ def test_ed_algorithm_3_with_left_padding():
     st = _run(wl, synth.checked_units(wl, wl.units), rule="recent", decode_bound=2, decode_p=1,
               accumulate=False)
     assert st.cuts == wl.units * wl.n_decode
+
+
+# --- a block and its cut in one call (fold + select + compaction fused) -----------
+@pytest.mark.parametrize("case", [
+    dict(name="c2-reduced", b=2, s=1024, n_decode=8),
+    dict(name="ragged", hh_mode="scatter", n_sinks=4, dtype="f32", b=2, n_heads=8, n_kv_heads=2,
+         head_dim=128, s=200, kv_max=70, block=33, n_decode=5),
+    dict(name="ragged", hh_mode="scatter", n_sinks=4, dtype="bf16", b=3, n_heads=8,
+         n_kv_heads=4, head_dim=64, s=300, kv_max=100, block=48, n_decode=5, pad_max=250),
+    # more than 4096 live entries: the call falls back to the separate kernels
+    dict(name="large", b=1, n_heads=4, n_kv_heads=1, s=6000, kv_max=4000, block=512, n_decode=2),
+], ids=lambda c: f"{c['name']}-{c.get('dtype', 'bf16')}-kv{c.get('kv_max', 512)}")
+def test_fused_block_cut(case):
+    wl = C2.with_(**case)
+    st = _run(wl, synth.checked_units(wl, wl.units), fused_cut=True)
+    assert st.cuts > 0
+
+
+@pytest.mark.parametrize("rule", ["sum", "tova"])
+def test_fused_block_cut_other_rules(rule):
+    wl = C2.with_(b=2, s=1024, n_decode=8)
+    _run(wl, synth.checked_units(wl, wl.units), fused_cut=True, rule=rule)

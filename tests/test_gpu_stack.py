@@ -4,7 +4,8 @@ The generator is checked word for word (raw Philox outputs) and element for
 element (Q/K/V rows, bf16 and float32) against the host evaluation of the same
 stream; the stack is checked against the float64 oracle on units spread over
 its first, middle and last layers, at the full per-unit shape (s = 8192, bound
-512, block 256, 256 decode steps) and a reduced batch.
+512, block 256, 256 decode steps), at a reduced batch and at the largest batch
+that fits the device (the benchmark's).
 """
 import sys
 
@@ -86,6 +87,36 @@ def test_c5_stack_parity_reduced_batch():
                (L - 2, 1, 6), (L // 4, 1, 1)]
     _say(f"[stack] {wl.name} b={wl.b} layers={L} s={wl.s} kv={wl.kv_max} B={wl.block} "
          f"D={wl.n_decode} units={checked}")
+    st = run_stack_parity(wl, checked)
+    _say(f"[stack] -> {st.summary()}")
+    assert not st.failures, "\n".join(st.failures)
+    assert st.cuts == len(checked) * (wl.s // wl.block - wl.kv_max // wl.block + wl.n_decode)
+
+
+def test_c5_stack_parity_full_batch():
+    """The 32-layer stack at the batch the benchmark runs (the largest that fits
+    the device), checked on sampled units of the first, middle and last layers
+    and of the first, middle and last samples."""
+    _need_gpu()
+    import gc
+
+    from paper_2412_05693_amd import batchmax as bmx
+    from pd_harness import run_stack_parity
+
+    gc.collect()
+    torch.cuda.empty_cache()
+    wl = synth.WORKLOADS["c5"]
+    shape = dict(n_layers=wl.n_layers, s=wl.s, kv_max=wl.kv_max, block=wl.block,
+                 max_gen=wl.n_decode, n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads,
+                 head_dim=wl.head_dim, dtype=wl.dtype)
+    free, _ = torch.cuda.mem_get_info()
+    b = bmx.plan_stack_batch(free - (3 << 30), **shape)
+    assert b >= 2, f"only {free / 1e9:.1f} GB free"
+    wl = wl.with_(b=b)
+    L = wl.n_layers
+    checked = [(0, 0, 0), (0, b - 1, 7), (L // 2, b // 2, 3), (L // 2, b - 1, 4),
+               (L - 1, 0, 5), (L - 1, b - 1, 2)]
+    _say(f"[stack] {wl.name} full batch b={b} layers={L} s={wl.s} units={checked}")
     st = run_stack_parity(wl, checked)
     _say(f"[stack] -> {st.summary()}")
     assert not st.failures, "\n".join(st.failures)

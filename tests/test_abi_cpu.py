@@ -123,6 +123,12 @@ def test_prefill_order_and_capacity_errors():
         assert status_of(bmx.bm_prefill_block, ctx, 192, 64, P, P, P, P, 32, 0) == bmx.BM_ERR_INVALID_ARG
         assert status_of(bmx.bm_prefill_block, ctx, 192, 64, 0, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
         assert status_of(bmx.bm_prefill_block, ctx, 192, 64, P + 2, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
+        # the fused block-and-cut call runs the same checks before any launch
+        cut = bmx.bm_prefill_block_cut
+        assert status_of(cut, ctx, 100, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
+        assert status_of(cut, ctx, 192, 0, P, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(cut, ctx, 192, 65, P, P, P, P, 65, 0) == bmx.BM_ERR_INVALID_ARG
+        assert status_of(cut, ctx, 192, 64, 0, P, P, P, 64, 0) == bmx.BM_ERR_INVALID_ARG
         assert bmx.bm_ctx_next_pos(ctx) == 192 and bmx.bm_ctx_len(ctx) == 128
     finally:
         bmx.bm_destroy(ctx)
@@ -136,6 +142,7 @@ def test_prefill_order_and_capacity_errors():
     ctx = _ctx(d, 192, 192)
     try:
         assert status_of(bmx.bm_prefill_block, ctx, 192, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
+        assert status_of(bmx.bm_prefill_block_cut, ctx, 192, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
         assert status_of(bmx.bm_evict_compact, ctx, 190, 0) == bmx.BM_ERR_ORDER
     finally:
         bmx.bm_destroy(ctx)
@@ -232,6 +239,7 @@ def test_decode_removal_beyond_the_decode_bound_is_rejected_before_launch():
 def test_null_context():
     P = FAKE
     assert status_of(bmx.bm_prefill_block, None, 0, 1, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_prefill_block_cut, None, 0, 1, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
     assert status_of(bmx.bm_evict_compact, None, 0, 0) == bmx.BM_ERR_INVALID_ARG
     assert status_of(bmx.bm_decode_step, None, 0, P, P, P, P, 1, 0) == bmx.BM_ERR_INVALID_ARG
     assert bmx.bm_ctx_len(None) == -1 and bmx.bm_ctx_next_pos(None) == -1
@@ -310,3 +318,17 @@ def test_padded_prefill_flops():
             bmx.prefill_flops(b=1, s=320 - 32 * k, **kw)
     f = [bmx.prefill_flops_padded(pads=[p], s=300, **kw) for p in range(0, 300, 7)]
     assert all(a >= b for a, b in zip(f, f[1:]))
+
+
+def test_fused_cut_refuses_an_unscored_cut():
+    # outputs-only prefill leaves no scores to rank by: a block whose cut is due
+    # is refused before any launch unless the rule ignores scores
+    d = dims()
+    ctx = _ctx(d, 128, 192)
+    P = FAKE
+    try:
+        bmx.bm_set_score_accumulation(ctx, 0)
+        assert status_of(bmx.bm_prefill_block_cut, ctx, 192, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
+        assert bmx.bm_ctx_len(ctx) == 128 and bmx.bm_ctx_next_pos(ctx) == 192
+    finally:
+        bmx.bm_destroy(ctx)

@@ -219,6 +219,9 @@ def test_ed_algorithm_3_with_left_padding():
          head_dim=128, s=200, kv_max=70, block=33, n_decode=5),
     dict(name="ragged", hh_mode="scatter", n_sinks=4, dtype="bf16", b=3, n_heads=8,
          n_kv_heads=4, head_dim=64, s=300, kv_max=100, block=48, n_decode=5, pad_max=250),
+    # exactly 4096 live entries before each cut: the fused kernel's largest LDS
+    # footprint (80 KB of slot arrays)
+    dict(name="edge", b=2, n_heads=8, n_kv_heads=2, s=4352, kv_max=3840, block=256, n_decode=3),
     # more than 4096 live entries: the call falls back to the separate kernels
     dict(name="large", b=1, n_heads=4, n_kv_heads=1, s=6000, kv_max=4000, block=512, n_decode=2),
 ], ids=lambda c: f"{c['name']}-{c.get('dtype', 'bf16')}-kv{c.get('kv_max', 512)}")

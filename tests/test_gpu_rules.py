@@ -235,3 +235,13 @@ def test_fused_block_cut(case):
 def test_fused_block_cut_other_rules(rule):
     wl = C2.with_(b=2, s=1024, n_decode=8)
     _run(wl, synth.checked_units(wl, wl.units), fused_cut=True, rule=rule)
+
+
+def test_fused_block_cut_outputs_only_recent_rule():
+    # outputs-only prefill (no score sums) with cuts by recency inside the
+    # fused call: the kernel folds nothing and keeps the newest entries
+    wl = C2.with_(name="ragged", hh_mode="scatter", n_sinks=4, b=2, n_heads=8, n_kv_heads=2,
+                  head_dim=128, s=300, kv_max=100, block=48, n_decode=4)
+    st = _run(wl, synth.checked_units(wl, wl.units), fused_cut=True, rule="recent",
+              accumulate=False)
+    assert st.cuts > 0

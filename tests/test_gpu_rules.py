@@ -245,3 +245,10 @@ def test_fused_block_cut_outputs_only_recent_rule():
     st = _run(wl, synth.checked_units(wl, wl.units), fused_cut=True, rule="recent",
               accumulate=False)
     assert st.cuts > 0
+
+
+def test_fused_block_cut_c3_shape():
+    # block 512 and bound 1024: 16 workgroups per unit fold into each cut
+    wl = synth.WORKLOADS["c3"].with_(b=2, s=2048, n_decode=4)
+    st = _run(wl, synth.checked_units(wl, wl.units), fused_cut=True)
+    assert st.cuts > 0

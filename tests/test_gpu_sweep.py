@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 RULES = ("ave", "sum", "recent", "tova")
 
 
-def _cases(n=32, seed=2412):
+def _cases(n=64, seed=2412):
     rng = np.random.default_rng(seed)
     out = []
     for i in range(n):

@@ -283,14 +283,15 @@ def decode_bytes(bmx, wl, b):
     return total
 
 
-def fused_label(dom, fused_cut):
-    """Name of the timed launch pair: with the fused cut a prefill bracket spans
-    the attention kernel and the fold/cut kernel, so its rate is the pair's (and
-    the attention kernel's counter records do not describe it)."""
-    return "prefill_attention+fold_cut" if fused_cut and dom == "prefill_attention" else dom
+def cut_kernel_entry(ms, launches, fused_cut):
+    """Timing of the launches that follow each block's attention kernel: the
+    fused fold/select/compaction kernel, or the score fold plus the separate
+    select and compaction kernels."""
+    return {"kernel": "fold_cut" if fused_cut else "score_reduce+select+compact",
+            "ms_per_step": ms, "launches_per_step": launches}
 
 
-def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cut=False):
+def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cut=True):
     import torch
 
     from paper_2412_05693_amd import batchmax as bmx
@@ -310,23 +311,24 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cu
         pd.set_left_padding(torch.from_numpy(pads).to(dev))
     stream = torch.cuda.current_stream(dev)
     blocks = [(t0, min(wl.block, wl.s - t0)) for t0 in range(0, wl.s, wl.block)]
+    mk = lambda: torch.cuda.Event(enable_timing=True)
 
     def one_step(ev=None):
+        # per block: [start] attention [split] fold/cut [end]; the split event
+        # is recorded by the library between its launches
         pd.reset()
         for bi_, (t0, n) in enumerate(blocks):
             if ev is not None:
-                ev["pf"][bi_][0].record(stream)
-            if fused_cut:      # block and cut in one call: timed together as prefill
+                pd.set_split_event(ev["split"][bi_])
+                ev["start"][bi_].record(stream)
+            if fused_cut:
                 pd.prefill_block_cut(t0, n, q, k, v, o)
             else:
                 pd.prefill_block(t0, n, q, k, v, o)
-            if ev is not None:
-                ev["pf"][bi_][1].record(stream)
-                ev["ev"][bi_][0].record(stream)
-            if not fused_cut:
                 pd.evict_compact(t0 + n - 1)
             if ev is not None:
-                ev["ev"][bi_][1].record(stream)
+                ev["end"][bi_].record(stream)
+        pd.set_split_event(None)
         if ev is not None:
             ev["dec"][0].record(stream)
         run_decode_loop()
@@ -334,9 +336,8 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cu
             ev["dec"][1].record(stream)
 
     def new_events():
-        mk = lambda: torch.cuda.Event(enable_timing=True)
-        return {"pf": [(mk(), mk()) for _ in blocks], "ev": [(mk(), mk()) for _ in blocks],
-                "dec": (mk(), mk())}
+        return {"start": [mk() for _ in blocks], "split": [mk() for _ in blocks],
+                "end": [mk() for _ in blocks], "dec": (mk(), mk())}
 
     def run_decode_loop():
         for t in range(wl.n_decode):
@@ -360,13 +361,13 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cu
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    pf_ms = sum(a.elapsed_time(b) for e in evs for (a, b) in e["pf"]) / steps
-    ev_ms = sum(a.elapsed_time(b) for e in evs for (a, b) in e["ev"]) / steps
+    nb = len(blocks)
+    pf_ms = sum(e["start"][i].elapsed_time(e["split"][i]) for e in evs for i in range(nb)) / steps
+    ev_ms = sum(e["split"][i].elapsed_time(e["end"][i]) for e in evs for i in range(nb)) / steps
     dec_ms = sum(e["dec"][0].elapsed_time(e["dec"][1]) for e in evs) / steps
     ms_step = wall * 1e3 / steps
 
     G = wl.group
-    es = 4 if wl.dtype == "f32" else 2
     if wl.pad_max > 0:
         flops = bmx.prefill_flops_padded(pads=pads, n_kv_heads=wl.n_kv_heads, group=G,
                                          head_dim=wl.head_dim, s=wl.s, kv_max=wl.kv_max,
@@ -378,30 +379,35 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cu
     peak_f = PEAK_F32_MFMA if wl.dtype == "f32" else PEAK_BF16_MFMA
     prefill_tflops = flops / (pf_ms * 1e-3) / 1e12
     decode_gbs = dbytes / (dec_ms * 1e-3) / 1e9 if wl.n_decode else 0.0
+    cut_bytes = cut_fixed_bytes(wl, wl.b) if fused_cut else None
     kernels = {
         "prefill_attention": {"bound": "mfma", "achieved": prefill_tflops,
                               "peak": peak_f / 1e12, "unit": "TFLOP/s",
                               "frac": prefill_tflops / (peak_f / 1e12),
-                              "ms_per_step": pf_ms, "launches_per_step": len(blocks),
-                              "algorithmic_per_launch": flops / len(blocks)},
-        "evict_compact": {"ms_per_step": ev_ms, "launches_per_step": len(blocks)},
+                              "ms_per_step": pf_ms, "launches_per_step": nb,
+                              "algorithmic_per_launch": flops / nb},
+        "evict_compact": cut_kernel_entry(ev_ms, nb, fused_cut),
         "decode_step": {"bound": "hbm", "achieved": decode_gbs, "peak": PEAK_HBM / 1e9,
                         "unit": "GB/s", "frac": decode_gbs / (PEAK_HBM / 1e9),
                         "ms_per_step": dec_ms, "launches_per_step": wl.n_decode,
                         "algorithmic_per_launch": dbytes / max(wl.n_decode, 1)},
     }
+    if cut_bytes is not None:
+        kernels["evict_compact"].update(cut_roofline(cut_bytes, ev_ms))
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd = kernels[dom]
     traffic = (measured_traffic(wl.name)
-               if dom == "prefill_attention" and counters_apply(wl) and not fused_cut else None)
+               if dom == "prefill_attention" and counters_apply(wl) else None)
     roofline = {"bound": kd["bound"], "achieved": round(kd["achieved"], 3), "peak": kd["peak"],
                 "unit": kd["unit"], "frac": round(kd["frac"], 5), "traffic": traffic,
-                "kernel": fused_label(dom, fused_cut)}
+                "kernel": dom}
     prompt_tokens = int(wl.b * wl.s - pads.sum())        # real tokens only (Sec. 3 padding)
     tokens = prompt_tokens + wl.b * wl.n_decode
     return {
         "value": tokens / (ms_step * 1e-3),
         "ms_per_step": ms_step,
+        "steps": steps,
+        "warmup": warmup,
         "roofline": roofline,
         "kernels": kernels,
         "phases": {"prefill_tokens_per_s": prompt_tokens / ((pf_ms + ev_ms) * 1e-3),
@@ -411,14 +417,71 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cu
     }
 
 
+def cut_fixed_bytes(wl, b) -> int:
+    """HBM bytes of one prefill step's fused fold/cut launches that do not
+    depend on the data: every live slot's partial column sums (one row per
+    attention workgroup that saw the slot), its score read and written and its
+    position read.  The moved K/V rows come on top (their number depends on
+    which entries the rule removes)."""
+    from paper_2412_05693_amd import batchmax as bmx
+
+    ppw = bmx.bm_prefill_positions_per_workgroup(bmx.make_dims(
+        b=1, s=wl.s, kv_max=wl.kv_max, block=wl.block, max_gen=wl.n_decode,
+        n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim, dtype=wl.dtype))
+    total = 0
+    length = 0
+    for t0 in range(0, wl.s, wl.block):
+        n = min(wl.block, wl.s - t0)
+        npt = -(-n // ppw)
+        part = length * npt + sum(npt - r // ppw for r in range(n))
+        live = length + n
+        total += 4 * part + 12 * live
+        length = min(wl.kv_max, live)
+    return total * b * wl.n_kv_heads
+
+
+def cut_roofline(nbytes, ms):
+    gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+    return {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+            "frac": gbs / (PEAK_HBM / 1e9), "algorithmic_bytes_per_step": nbytes,
+            "algorithmic_basis": "partial sums, scores and positions only (moved rows excluded)"}
+
+
 STACK_RESERVE = 3 << 30      # device bytes left to the runtime when planning the batch
+STACK_TIMED_BUDGET_S = 90.0  # wall seconds of timed layer-stack passes (default)
 
 
-def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm", fused_cut=False):
+def profiler_attached() -> bool:
+    """rocprofv3 exports ROCPROF_* variables to the program it profiles."""
+    return any(k.startswith("ROCPROF_") for k in os.environ)
+
+
+def stack_warmup(requested: int) -> int:
+    """Untimed layer-stack passes actually run: at most one (a pass is tens of
+    seconds and the first one already warms every kernel and the allocator)."""
+    return min(max(requested, 0), 1)
+
+
+def more_stack_passes(done: int, requested: int, elapsed_s: float, last_pass_s: float,
+                      budget_s: float) -> bool:
+    """Time another layer-stack pass?  Always at least one; never more than
+    requested; otherwise only while the next pass (taken to last as long as the
+    previous one) still ends inside the wall budget."""
+    if done < 1:
+        return True
+    if done >= requested:
+        return False
+    return elapsed_s + last_pass_s <= budget_s
+
+
+def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm", fused_cut=True,
+                    budget_s=STACK_TIMED_BUDGET_S):
     """The layer stack at the largest batch that fits: per (layer, block) the
     device generator writes the block's Q/K/V, then prefill and the cut; then
     the decode steps, layer by layer.  Generator time is measured and left out
-    of the throughput (the inputs of a resident workload are not generated)."""
+    of the throughput (the inputs of a resident workload are not generated).
+    Timed passes stop at ``steps`` or when the next one would end past
+    ``budget_s`` seconds of timed wall time, whichever comes first."""
     import torch
 
     from paper_2412_05693_amd import batchmax as bmx
@@ -485,11 +548,26 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm", fus
             for layer in range(L):
                 pd = stack.layers[layer]
                 rec("gen", lambda: bmx.synth_qkv(params[layer], t0, q, k, v))
-                if fused_cut:   # block and cut in one call: timed together as prefill
-                    rec("pf", lambda: pd.prefill_block_cut(t0, n, q, k, v, o, row=0))
+                if ev is None:
+                    if fused_cut:
+                        pd.prefill_block_cut(t0, n, q, k, v, o, row=0)
+                    else:
+                        pd.prefill_block(t0, n, q, k, v, o, row=0)
+                        pd.evict_compact(t0 + n - 1)
+                    continue
+                # [start] attention [split] fold/cut [end]
+                a, sp, z = mk(), mk(), mk()
+                pd.set_split_event(sp)
+                a.record(stream)
+                if fused_cut:
+                    pd.prefill_block_cut(t0, n, q, k, v, o, row=0)
                 else:
-                    rec("pf", lambda: pd.prefill_block(t0, n, q, k, v, o, row=0))
-                    rec("cut", lambda: pd.evict_compact(t0 + n - 1))
+                    pd.prefill_block(t0, n, q, k, v, o, row=0)
+                    pd.evict_compact(t0 + n - 1)
+                z.record(stream)
+                pd.set_split_event(None)
+                ev["pf"].append((a, sp))
+                ev["cut"].append((sp, z))
         for t in range(wl.n_decode):
             p = wl.s + t
             for layer in range(L):
@@ -498,22 +576,27 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm", fus
                 rec("dec", lambda: pd.decode_step(p, qd, kd, vd, od, row=0))
         return ev
 
-    for _ in range(warmup):
+    warm = stack_warmup(warmup)
+    for i in range(warm):
+        t0w = time.perf_counter()
         one_step(False)
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        print(f"[bench] warm-up pass {i + 1}/{warm}: {time.perf_counter() - t0w:.1f} s", flush=True)
     evs, walls = [], []
-    for _ in range(steps):
+    while more_stack_passes(len(walls), steps, sum(walls), walls[-1] if walls else 0.0, budget_s):
         torch.cuda.synchronize()
         t0w = time.perf_counter()
         evs.append(one_step(True))
         torch.cuda.synchronize()
         walls.append(time.perf_counter() - t0w)
+        print(f"[bench] timed pass {len(walls)}: {walls[-1]:.1f} s", flush=True)
+    done = len(walls)
 
     def ms(kind):
-        return sum(a.elapsed_time(z) for e in evs for (a, z) in e[kind]) / steps
+        return sum(a.elapsed_time(z) for e in evs for (a, z) in e[kind]) / done
 
     gen_ms, pf_ms, ev_ms, dec_ms = ms("gen"), ms("pf"), ms("cut"), ms("dec")
-    wall_ms = sum(walls) * 1e3 / steps
+    wall_ms = sum(walls) * 1e3 / done
     ms_step = wall_ms - gen_ms
     G = wl.group
     flops = L * bmx.prefill_flops(b=b, n_kv_heads=Hk, group=G, head_dim=d, s=wl.s,
@@ -529,37 +612,42 @@ def gpu_bench_stack(name, overrides, steps, warmup, batch=None, method="bm", fus
                               "frac": prefill_tflops / (peak_f / 1e12),
                               "ms_per_step": pf_ms, "launches_per_step": n_pf,
                               "algorithmic_per_launch": flops / n_pf},
-        "evict_compact": {"ms_per_step": ev_ms, "launches_per_step": n_pf},
+        "evict_compact": cut_kernel_entry(ev_ms, n_pf, fused_cut),
         "decode_step": {"bound": "hbm", "achieved": decode_gbs, "peak": PEAK_HBM / 1e9,
                         "unit": "GB/s", "frac": decode_gbs / (PEAK_HBM / 1e9),
                         "ms_per_step": dec_ms, "launches_per_step": L * wl.n_decode,
                         "algorithmic_per_launch": dbytes / (L * max(wl.n_decode, 1))},
     }
+    if fused_cut:
+        kernels["evict_compact"].update(cut_roofline(L * cut_fixed_bytes(wl, b), ev_ms))
     dom = "prefill_attention" if pf_ms >= dec_ms else "decode_step"
     kd_ = kernels[dom]
     traffic = (measured_traffic(wl.name, b * Hk)
-               if dom == "prefill_attention" and counters_apply(wl) and not fused_cut else None)
+               if dom == "prefill_attention" and counters_apply(wl) else None)
     roofline = {"bound": kd_["bound"], "achieved": round(kd_["achieved"], 3), "peak": kd_["peak"],
                 "unit": kd_["unit"], "frac": round(kd_["frac"], 5), "traffic": traffic,
-                "kernel": fused_label(dom, fused_cut)}
+                "kernel": dom}
     if traffic is not None:
         roofline["traffic_basis"] = ("FETCH_SIZE/WRITE_SIZE per unit of the same launches "
                                      "measured on c2, scaled to this launch's units")
     tokens = b * (wl.s + wl.n_decode)
-    stack.close()
     return {
         "value": tokens / (ms_step * 1e-3),
         "ms_per_step": ms_step,
+        "steps": done,
+        "warmup": warm,
         "roofline": roofline,
         "kernels": kernels,
         "phases": {"prefill_tokens_per_s": b * wl.s / ((pf_ms + ev_ms) * 1e-3),
                    "decode_tokens_per_s": b * wl.n_decode / (dec_ms * 1e-3),
                    "generated_tokens_per_s": b * wl.n_decode / (ms_step * 1e-3),
                    "input_generation_ms_per_step": gen_ms,
-                   "wall_ms_per_step_with_generation": wall_ms},
+                   "wall_ms_per_step_with_generation": wall_ms,
+                   "timed_wall_s": sum(walls), "timed_wall_budget_s": budget_s},
         "stack": {"n_layers": L, "max_batch": b_plan, "max_batch_decoding_only": b_do,
                   "device_free_bytes": free, "arena_bytes": stack.arena_bytes},
         "workload": wl,
+        "close": stack.close,
     }
 
 
@@ -567,9 +655,13 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
-                    help="timed steps (default 10; 1 for the layer stack)")
+                    help="timed steps (default 10; for the layer stack at most this many, "
+                         "within --time-budget)")
     ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed steps first (default 2; 1 for the layer stack)")
+                    help="untimed steps first (default 2; the layer stack runs at most 1)")
+    ap.add_argument("--time-budget", type=float, default=STACK_TIMED_BUDGET_S,
+                    help="layer stack: wall seconds of timed passes; no pass starts that "
+                         "would end past it (at least one always runs)")
     ap.add_argument("--config", default="c5", choices=["c1", "c2", "c3", "c4", "c5"],
                     help="workload (default c5: the 32-layer stack at the largest batch that "
                          "fits, the configuration the metric is quoted at)")
@@ -590,9 +682,9 @@ def main():
     ap.add_argument("--pad-max", type=int, default=0,
                     help="single-layer workloads: left-pad sample j by pad_j in [0, N] tokens "
                          "(per-sample prompt lengths s - pad_j, Sec. 3); value counts real tokens")
-    ap.add_argument("--fused-cut", action="store_true",
-                    help="run each prefill block and its cut as one call (fold, select and "
-                         "compaction in one kernel); prefill timings then include the cut")
+    ap.add_argument("--separate-cut", action="store_true",
+                    help="cut each block with the score fold, select and compaction kernels "
+                         "(three launches) instead of the fused fold/cut kernel (the default)")
     ap.add_argument("--graph", action="store_true",
                     help="single-layer workloads: replay the decode loop as one HIP graph")
     ap.add_argument("--peak-probe", action="store_true",
@@ -616,6 +708,12 @@ def main():
               "the path shards with no communication and is not run across GPUs here.",
               file=sys.stderr)
         sys.exit(2)
+    if stack and not args.batch and profiler_attached():
+        # Three profiler runs of the full-batch stack ended in a host-side crash
+        # inside the profiler's launch interception; profile a given --batch.
+        print("bench.py: the layer stack at the largest batch that fits is not run under a "
+              "profiler; pass --batch N", file=sys.stderr)
+        sys.exit(2)
 
     overrides = {"decode_p": args.decode_p} if args.decode_p else {}
     if args.rule != "ave":
@@ -628,15 +726,17 @@ def main():
             print("bench.py: --pad-max applies to the single-layer workloads", file=sys.stderr)
             sys.exit(2)
         overrides["pad_max"] = args.pad_max
+    fused_cut = not args.separate_cut
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, overrides, args.cpu_seconds, args.method)
-    if args.config == "c5":
+    if stack:
         res = gpu_bench_stack(args.config, overrides, args.steps, args.warmup, args.batch,
-                              method=args.method, fused_cut=args.fused_cut)
+                              method=args.method, fused_cut=fused_cut,
+                              budget_s=args.time_budget)
     else:
         res = gpu_bench(args.config, overrides, args.steps, args.warmup, method=args.method,
-                        graph=args.graph, fused_cut=args.fused_cut)
+                        graph=args.graph, fused_cut=fused_cut)
     wl = res["workload"]
     line = {
         "metric": ("P&D tokens/s (prefill+decode) at max batch; prefill MFMA %, decode HBM GB/s"
@@ -644,8 +744,10 @@ def main():
         "value": round(res["value"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": res["steps"],
+        "warmup": res["warmup"],
+        "steps_requested": args.steps,
+        "warmup_requested": args.warmup,
         "ms_per_step": round(res["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -659,8 +761,8 @@ def main():
                                       else "one per step"),
                    "left_pad_max": wl.pad_max,
                    "rank_rule": wl.rule,
-                   "decode_graph": bool(args.graph and args.config != "c5"),
-                   "fused_cut": bool(args.fused_cut),
+                   "decode_graph": bool(args.graph and not stack),
+                   "fused_cut": fused_cut,
                    "method": {"bm": "Batch-Max (Algorithm 1)",
                               "ed": "extreme decoding-only (Algorithm 3)",
                               "fkv": "full KV cache"}[args.method],
@@ -675,6 +777,8 @@ def main():
         line["config"]["max_batch_decoding_only"] = res["stack"]["max_batch_decoding_only"]
         line["stack"] = res["stack"]
     print(json.dumps(line), flush=True)
+    if "close" in res:
+        res["close"]()
 
 
 if __name__ == "__main__":

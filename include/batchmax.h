@@ -124,6 +124,12 @@ const char* bm_last_error(void);
 /* cap = kv_max + block slots per unit; -1 if dims are invalid. */
 int32_t bm_cache_slots(const bm_dims* dims);
 
+/* Block positions one prefill attention workgroup covers (all G heads of a
+ * unit): a block of n_tok tokens runs ceil(n_tok / this) workgroups per unit,
+ * each writing one row of partial score sums per live slot it sees.  -1 if
+ * dims are invalid. */
+int32_t bm_prefill_positions_per_workgroup(const bm_dims* dims);
+
 /* Bytes of bm_cache.work the calls need; 0 if dims are invalid. */
 size_t bm_workspace_bytes(const bm_dims* dims);
 
@@ -237,6 +243,16 @@ int bm_set_left_padding(bm_ctx* ctx, const int32_t* pad);
  * BM_ERR_ORDER (its scores would miss that block) until the context is
  * rebuilt. */
 int bm_set_score_accumulation(bm_ctx* ctx, int32_t on);
+
+/* Instrumentation (no effect on results): when `event` is not null, every
+ * later bm_prefill_block and bm_prefill_block_cut records it on its stream
+ * right after the block's attention kernel and before the launches that fold
+ * the score sums (and, for bm_prefill_block_cut, cut and compact), so a caller
+ * can time the attention and the cut separately with events on one stream.
+ * The event is caller-owned and must stay valid while set; null turns the
+ * hook off.  BM_ERR_INVALID_ARG for a null context; a failed record returns
+ * BM_ERR_HIP from the prefill call. */
+int bm_set_split_event(bm_ctx* ctx, hipEvent_t event);
 
 /* Host copies of the uniform cache length and of the next expected position
  * (-1 for a null context). */

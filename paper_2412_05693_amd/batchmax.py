@@ -75,6 +75,7 @@ def _load() -> ctypes.CDLL:
         "bm_last_error": (ctypes.c_char_p, []),
         "bm_cache_slots": (I32, [dims_p]),
         "bm_workspace_bytes": (SZ, [dims_p]),
+        "bm_prefill_positions_per_workgroup": (I32, [dims_p]),
         "bm_validate_dims": (ctypes.c_int, [dims_p]),
         "bm_init": (ctypes.c_int, [dims_p, cache_p, P, ctypes.POINTER(P)]),
         "bm_resume": (ctypes.c_int, [dims_p, cache_p, I32, I32, ctypes.POINTER(P)]),
@@ -86,6 +87,7 @@ def _load() -> ctypes.CDLL:
         "bm_set_decode_bound": (ctypes.c_int, [P, I32]),
         "bm_set_score_accumulation": (ctypes.c_int, [P, I32]),
         "bm_set_left_padding": (ctypes.c_int, [P, P]),
+        "bm_set_split_event": (ctypes.c_int, [P, P]),
         "bm_decode_step": (ctypes.c_int, [P, I32, P, P, P, P, I32, P]),
         "bm_ctx_len": (I32, [P]),
         "bm_ctx_next_pos": (I32, [P]),
@@ -102,10 +104,11 @@ def _load() -> ctypes.CDLL:
 
 _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
+            "bm_prefill_positions_per_workgroup",
             "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block",
             "bm_prefill_block_cut", "bm_evict_compact",
             "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
-            "bm_set_score_accumulation", "bm_set_left_padding",
+            "bm_set_score_accumulation", "bm_set_left_padding", "bm_set_split_event",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
             "bm_philox4x32_10")
 
@@ -132,6 +135,10 @@ def bm_cache_slots(dims: bm_dims) -> int:
 
 def bm_workspace_bytes(dims: bm_dims) -> int:
     return _lib.bm_workspace_bytes(ctypes.byref(dims))
+
+
+def bm_prefill_positions_per_workgroup(dims: bm_dims) -> int:
+    return _lib.bm_prefill_positions_per_workgroup(ctypes.byref(dims))
 
 
 def bm_validate_dims(dims: bm_dims) -> None:
@@ -183,6 +190,10 @@ def bm_set_score_accumulation(ctx: int, on: int) -> None:
 
 def bm_set_left_padding(ctx: int, pad_ptr: int) -> None:
     _check(_lib.bm_set_left_padding(ctx, pad_ptr))
+
+
+def bm_set_split_event(ctx: int, event: int) -> None:
+    _check(_lib.bm_set_split_event(ctx, event))
 
 
 def bm_decode_step(ctx: int, pos: int, q: int, k: int, v: int, o: int, seq_ld: int,
@@ -298,7 +309,7 @@ class PDAttention:
     # -- schedule ---------------------------------------------------------------
     _SETTERS = {"removal": bm_set_decode_removal, "rule": bm_set_rank_rule,
                 "bound": bm_set_decode_bound, "accumulate": bm_set_score_accumulation,
-                "pad": bm_set_left_padding}
+                "pad": bm_set_left_padding, "split": bm_set_split_event}
 
     def _apply_settings(self) -> None:
         for key, val in self._settings.items():
@@ -375,6 +386,19 @@ class PDAttention:
             raise ValueError(f"pads: need a contiguous int32 [{self.dims.b}] tensor on {self.device}")
         self._pads = pads
         self._set("pad", pads.data_ptr())
+
+    def set_split_event(self, event) -> None:
+        """Record ``event`` (a torch.cuda.Event, or None to stop) between each
+        later prefill block's attention kernel and its fold/cut launches, so the
+        two can be timed separately on one stream.  The event is recorded once
+        here on the current stream so that it exists."""
+        if event is None:
+            self._split = None
+            self._set("split", None)
+            return
+        event.record(self.torch.cuda.current_stream(self.device))
+        self._split = event
+        self._set("split", event.cuda_event)
 
     def decode_step(self, pos, q, k, v, o, row=0) -> None:
         H, Hk = self.dims.n_heads, self.dims.n_kv_heads

@@ -30,6 +30,7 @@ struct bm_ctx {
   bool accumulate;    // prefill adds probabilities to the scores
   bool scores_valid;  // no block has run without accumulation
   const int32_t* pad; // device [b] left pad tokens per sample, or null
+  hipEvent_t split;   // recorded between a block's attention and its score/cut launches, or null
 };
 
 namespace {
@@ -135,6 +136,11 @@ BM_EXPORT int32_t bm_cache_slots(const bm_dims* dims) {
   return dims->kv_max + dims->block;
 }
 
+BM_EXPORT int32_t bm_prefill_positions_per_workgroup(const bm_dims* dims) {
+  if (check_dims(dims) != BM_OK) return -1;
+  return bm::positions_per_wg(dims->n_heads / dims->n_kv_heads);
+}
+
 BM_EXPORT size_t bm_workspace_bytes(const bm_dims* dims) {
   if (check_dims(dims) != BM_OK) return 0;
   return bm::workspace_layout(*dims).total;
@@ -174,6 +180,7 @@ int make_ctx(const bm_dims* dims, const bm_cache* cache, bm_ctx** out) {
   c->accumulate = true;
   c->scores_valid = true;
   c->pad = nullptr;
+  c->split = nullptr;
   *out = c;
   return BM_OK;
 }
@@ -290,6 +297,8 @@ BM_EXPORT int bm_prefill_block(bm_ctx* ctx, int32_t t0, int32_t n_tok, const voi
   if (st != BM_OK) return st;
   hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  if (ctx->split && (e = hipEventRecord(ctx->split, stream)) != hipSuccess)
+    return hip_fail(e, "split event record");
   e = bm::launch_score_reduce(a, stream);
   if (e != hipSuccess) return hip_fail(e, "score reduce launch");
   advance(ctx, t0, n_tok);
@@ -309,6 +318,8 @@ BM_EXPORT int bm_prefill_block_cut(bm_ctx* ctx, int32_t t0, int32_t n_tok, const
                 "a block ran without score accumulation: only BM_RANK_RECENT can rank this cache");
   hipError_t e = bm::launch_prefill(a, ctx->dims.dtype, ctx->dims.head_dim, ctx->group, stream);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  if (ctx->split && (e = hipEventRecord(ctx->split, stream)) != hipSuccess)
+    return hip_fail(e, "split event record");
   if (n > bm::kMaxCap) {
     // too many entries for the one-workgroup cut: fold, then the two-kernel cut
     e = bm::launch_score_reduce(a, stream);
@@ -425,6 +436,12 @@ BM_EXPORT int bm_set_left_padding(bm_ctx* ctx, const int32_t* pad) {
   if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
   if ((uintptr_t)pad & 3) return fail(BM_ERR_INVALID_ARG, "pad must be 4-byte aligned");
   ctx->pad = pad;
+  return ok();
+}
+
+BM_EXPORT int bm_set_split_event(bm_ctx* ctx, hipEvent_t event) {
+  if (!ctx) return fail(BM_ERR_INVALID_ARG, "ctx is null");
+  ctx->split = event;
   return ok();
 }
 

@@ -61,6 +61,9 @@ def test_slots_and_workspace():
     U, cap, npt = 4, 192, 2
     assert ws >= U * npt * cap * 4 + 2 * U * cap * 4 + U * 4
     assert bmx.bm_cache_slots(dims(b=0)) == -1
+    assert bmx.bm_prefill_positions_per_workgroup(d) == 128 // 4
+    assert bmx.bm_prefill_positions_per_workgroup(dims(n_heads=2, n_kv_heads=2)) == 128
+    assert bmx.bm_prefill_positions_per_workgroup(dims(b=0)) == -1
     assert bmx.bm_workspace_bytes(dims(head_dim=96)) == 0
 
 
@@ -330,5 +333,16 @@ def test_fused_cut_refuses_an_unscored_cut():
         bmx.bm_set_score_accumulation(ctx, 0)
         assert status_of(bmx.bm_prefill_block_cut, ctx, 192, 64, P, P, P, P, 64, 0) == bmx.BM_ERR_ORDER
         assert bmx.bm_ctx_len(ctx) == 128 and bmx.bm_ctx_next_pos(ctx) == 192
+    finally:
+        bmx.bm_destroy(ctx)
+
+
+def test_split_event_hook():
+    d = dims()
+    assert status_of(bmx.bm_set_split_event, 0, 0) == bmx.BM_ERR_INVALID_ARG
+    ctx = _ctx(d, 0, 0)
+    try:
+        bmx.bm_set_split_event(ctx, FAKE)       # stored only; never recorded here
+        bmx.bm_set_split_event(ctx, None)
     finally:
         bmx.bm_destroy(ctx)

@@ -75,3 +75,70 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_stack_pass_budget():
+    # at most one untimed pass, whatever is requested
+    assert bench.stack_warmup(5) == 1 and bench.stack_warmup(1) == 1 and bench.stack_warmup(0) == 0
+    # the driver's request (--steps 20) with 35 s passes and a 90 s budget: 2 passes
+    done, walls = 0, []
+    while bench.more_stack_passes(done, 20, sum(walls), walls[-1] if walls else 0.0, 90.0):
+        walls.append(35.0)
+        done += 1
+    assert done == 2 and sum(walls) <= 90.0
+    # one pass always runs, even past the budget
+    assert bench.more_stack_passes(0, 20, 0.0, 0.0, 1.0)
+    assert not bench.more_stack_passes(1, 20, 500.0, 500.0, 1.0)
+    # never more than requested
+    assert not bench.more_stack_passes(3, 3, 1.0, 0.1, 1e9)
+    assert bench.more_stack_passes(2, 3, 1.0, 0.1, 1e9)
+
+
+def test_driver_command_fits_its_limit():
+    """The driver's `--steps 20 --warmup 5` on the stack: one warm-up pass and
+    the timed passes the budget allows, worst case (one timed pass of any
+    length is still taken) the pass time twice plus the budget."""
+    pass_s = 40.0                        # measured c5 pass with input generation: about 35 s
+    warm = bench.stack_warmup(5)
+    done, walls = 0, []
+    while bench.more_stack_passes(done, 20, sum(walls), walls[-1] if walls else 0.0,
+                                  bench.STACK_TIMED_BUDGET_S):
+        walls.append(pass_s)
+        done += 1
+    gpu_s = warm * pass_s + sum(walls)
+    assert gpu_s <= 300.0
+
+
+def test_profiler_guard(monkeypatch):
+    monkeypatch.delenv("ROCPROF_OUTPUT_PATH", raising=False)
+    for k in list(os.environ):
+        if k.startswith("ROCPROF_"):
+            monkeypatch.delenv(k)
+    assert not bench.profiler_attached()
+    monkeypatch.setenv("ROCPROF_OUTPUT_PATH", "/tmp/x")
+    assert bench.profiler_attached()
+
+
+def test_full_batch_stack_refused_under_a_profiler():
+    env = dict(os.environ, ROCPROF_OUTPUT_PATH="/tmp/none")
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--no-cpu-baseline"],
+                       capture_output=True, text=True, timeout=120, env=env)
+    assert r.returncode == 2 and "--batch" in r.stderr
+
+
+def test_cut_fixed_bytes():
+    """Fused fold/cut bytes per step: per block, each live slot's partial rows
+    (one per attention workgroup that saw it) plus score read/write and
+    position read, checked by hand on a two-block case."""
+    wl = synth.WORKLOADS["c2"].with_(b=1, s=512, kv_max=256, block=256)
+    d = bmx.make_dims(b=1, s=512, kv_max=256, block=256, max_gen=wl.n_decode, n_heads=32,
+                      n_kv_heads=8, head_dim=128, dtype="bf16")
+    ppw = bmx.bm_prefill_positions_per_workgroup(d)
+    assert ppw == 128 // wl.group
+    npt = 256 // ppw
+    # block 0: no cache; block row r is seen by the workgroups pt >= r // ppw
+    b0 = sum(npt - r // ppw for r in range(256))
+    # block 1: 256 cached slots seen by every workgroup, then the block rows
+    b1 = 256 * npt + b0
+    want = (4 * b0 + 12 * 256) + (4 * b1 + 12 * 512)
+    assert bench.cut_fixed_bytes(wl, 1) == want * wl.n_kv_heads

@@ -142,6 +142,26 @@ int bm_validate_dims(const bm_dims* dims);
  * `stream` the zeroing of len and score.  Next expected prefill position: 0. */
 int bm_init(const bm_dims* dims, const bm_cache* cache, hipStream_t stream, bm_ctx** out);
 
+/* Bytes of the library's static device workspace (bm_init_static_workspace). */
+#define BM_STATIC_WORKSPACE_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid allocation): bm_init, except
+ * that cache->work and cache->work_bytes are ignored and the context's
+ * workspace is the library's own static device array of
+ * BM_STATIC_WORKSPACE_BYTES, one per GPU (the current device's copy; it lives
+ * until the process ends).  The caller still owns k, v, score, pos and len.
+ * Nothing here or in later calls on the context allocates or frees memory.
+ * Every context made this way on one GPU shares that array and it keeps what
+ * the last call left in it (no call needs it cleared first): work enqueued by
+ * two such contexts that can overlap on one GPU -- concurrent streams or
+ * threads -- races and gives wrong results; work serialised on one stream is
+ * fine.  The current device must be the one `stream` runs on.
+ * BM_ERR_UNSUPPORTED if bm_workspace_bytes(dims) exceeds the static size
+ * (checked before any HIP call); otherwise as bm_init. */
+int bm_init_static_workspace(const bm_dims* dims, const bm_cache* cache, hipStream_t stream,
+                             bm_ctx** out);
+
 /* Create a context over a cache that already holds a valid state (for
  * example one restored from a snapshot): `len` live entries per unit (the same
  * for every unit) and `next_pos` the next position to process.  No device

@@ -78,6 +78,7 @@ def _load() -> ctypes.CDLL:
         "bm_prefill_positions_per_workgroup": (I32, [dims_p]),
         "bm_validate_dims": (ctypes.c_int, [dims_p]),
         "bm_init": (ctypes.c_int, [dims_p, cache_p, P, ctypes.POINTER(P)]),
+        "bm_init_static_workspace": (ctypes.c_int, [dims_p, cache_p, P, ctypes.POINTER(P)]),
         "bm_resume": (ctypes.c_int, [dims_p, cache_p, I32, I32, ctypes.POINTER(P)]),
         "bm_prefill_block": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
         "bm_prefill_block_cut": (ctypes.c_int, [P, I32, I32, P, P, P, P, I32, P]),
@@ -105,7 +106,7 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_bytes",
             "bm_prefill_positions_per_workgroup",
-            "bm_validate_dims", "bm_init", "bm_resume", "bm_prefill_block",
+            "bm_validate_dims", "bm_init", "bm_init_static_workspace", "bm_resume", "bm_prefill_block",
             "bm_prefill_block_cut", "bm_evict_compact",
             "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
             "bm_set_score_accumulation", "bm_set_left_padding", "bm_set_split_event",
@@ -148,6 +149,13 @@ def bm_validate_dims(dims: bm_dims) -> None:
 def bm_init(dims: bm_dims, cache: bm_cache, stream: int) -> int:
     out = ctypes.c_void_p()
     _check(_lib.bm_init(ctypes.byref(dims), ctypes.byref(cache), stream, ctypes.byref(out)))
+    return out.value
+
+
+def bm_init_static_workspace(dims: bm_dims, cache: bm_cache, stream: int) -> int:
+    out = ctypes.c_void_p()
+    _check(_lib.bm_init_static_workspace(ctypes.byref(dims), ctypes.byref(cache), stream,
+                                         ctypes.byref(out)))
     return out.value
 
 
@@ -241,7 +249,10 @@ class PDAttention:
     """
 
     def __init__(self, *, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim,
-                 dtype="bf16", sm_scale=0.0, device="cuda", init=True, buffers=None):
+                 dtype="bf16", sm_scale=0.0, device="cuda", init=True, buffers=None,
+                 static_workspace=False):
+        """``static_workspace``: no workspace tensor; contexts come from
+        bm_init_static_workspace and use the library's static device array."""
         import torch
 
         self.torch = torch
@@ -258,13 +269,17 @@ class PDAttention:
         self.group = n_heads // n_kv_heads
         U = b * n_kv_heads
         self.work_bytes = bm_workspace_bytes(self.dims)
+        self.static_workspace = static_workspace
+        if static_workspace and buffers is not None:
+            raise ValueError("static_workspace takes no caller buffers")
         if buffers is None:
             self.k = torch.empty((b, n_kv_heads, self.cap, head_dim), dtype=self.tdtype, device=self.device)
             self.v = torch.empty_like(self.k)
             self.score = torch.empty((b, n_kv_heads, self.cap), dtype=torch.float32, device=self.device)
             self.pos = torch.zeros((b, n_kv_heads, self.cap), dtype=torch.int32, device=self.device)
             self.len = torch.empty((b, n_kv_heads), dtype=torch.int32, device=self.device)
-            self.work = torch.empty(self.work_bytes, dtype=torch.uint8, device=self.device)
+            self.work = (None if static_workspace else
+                         torch.empty(self.work_bytes, dtype=torch.uint8, device=self.device))
         else:
             # caller-provided views (for example slices of one arena); shapes checked
             self.k, self.v, self.score, self.pos, self.len, self.work = buffers
@@ -278,8 +293,9 @@ class PDAttention:
             if self.work.numel() * self.work.element_size() < self.work_bytes:
                 raise ValueError("work buffer is smaller than bm_workspace_bytes")
         self.cache = bm_cache(self.k.data_ptr(), self.v.data_ptr(), self.score.data_ptr(),
-                              self.pos.data_ptr(), self.len.data_ptr(), self.work.data_ptr(),
-                              self.work_bytes)
+                              self.pos.data_ptr(), self.len.data_ptr(),
+                              0 if self.work is None else self.work.data_ptr(),
+                              0 if self.work is None else self.work_bytes)
         self.units = U
         self.ctx = None
         # schedule settings (bm_set_*): kept here and applied again to every new
@@ -324,10 +340,13 @@ class PDAttention:
         if self.ctx is not None:
             bm_destroy(self.ctx)
             self.ctx = None
-        self.ctx = bm_init(self.dims, self.cache, self._stream())
+        init = bm_init_static_workspace if self.static_workspace else bm_init
+        self.ctx = init(self.dims, self.cache, self._stream())
         self._apply_settings()
 
     def resume(self, length: int, next_pos: int) -> None:
+        if self.static_workspace:
+            raise ValueError("resume needs a caller-allocated workspace")
         if self.ctx is not None:
             bm_destroy(self.ctx)
             self.ctx = None

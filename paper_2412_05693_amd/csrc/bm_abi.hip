@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -203,6 +204,64 @@ BM_EXPORT int bm_init(const bm_dims* dims, const bm_cache* cache, hipStream_t st
   }
   *out = c;
   return ok();
+}
+
+// ---------------------------------------------------------------------------
+// the library's own workspace for callers that cannot allocate device memory
+// ---------------------------------------------------------------------------
+namespace {
+
+// Each GPU the library runs on holds its own copy of this array until the
+// process ends.  In host code `scratch` names a host-side stand-in, not the
+// device address: host code only ever uses the address hipGetSymbolAddress
+// returns for the current device.
+static __device__ __align__(256) char scratch[BM_STATIC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up once per
+// device (with that device current) and kept.
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(BM_ERR_UNSUPPORTED, "device %d beyond the %d the library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(BM_ERR_HIP, "hipGetSymbolAddress(scratch) returned null");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return BM_OK;
+}
+
+}  // namespace
+
+BM_EXPORT int bm_init_static_workspace(const bm_dims* dims, const bm_cache* cache,
+                                       hipStream_t stream, bm_ctx** out) {
+  if (out) *out = nullptr;
+  int st = check_dims(dims);
+  if (st != BM_OK) return st;
+  if (!cache || !out) return fail(BM_ERR_INVALID_ARG, "cache or out is null");
+  const size_t need = bm::workspace_layout(*dims).total;
+  if (need > (size_t)BM_STATIC_WORKSPACE_BYTES)
+    return fail(BM_ERR_UNSUPPORTED,
+                "workspace of %zu bytes exceeds the static workspace of %zu bytes: use bm_init "
+                "with a caller-allocated workspace",
+                need, (size_t)BM_STATIC_WORKSPACE_BYTES);
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != BM_OK) return st;
+  bm_cache c = *cache;
+  c.work = ws;
+  c.work_bytes = (size_t)BM_STATIC_WORKSPACE_BYTES;
+  return bm_init(dims, &c, stream, out);
 }
 
 BM_EXPORT int bm_resume(const bm_dims* dims, const bm_cache* cache, int32_t len,

@@ -346,3 +346,13 @@ def test_split_event_hook():
         bmx.bm_set_split_event(ctx, None)
     finally:
         bmx.bm_destroy(ctx)
+
+
+def test_static_workspace_refuses_oversized_dims_before_device_work():
+    # c4's shape needs about 200 MB of workspace, more than the static array
+    d = dims(b=1024, s=2048, kv_max=512, block=256, n_heads=32, n_kv_heads=8)
+    assert bmx.bm_workspace_bytes(d) > (64 << 20)
+    assert status_of(bmx.bm_init_static_workspace, d, fake_cache(d), 0) == bmx.BM_ERR_UNSUPPORTED
+    assert "static workspace" in bmx.bm_last_error()
+    assert status_of(bmx.bm_init_static_workspace, dims(b=0), fake_cache(d), 0) == \
+        bmx.BM_ERR_INVALID_ARG

@@ -19,7 +19,9 @@ import math
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libbatchmax.so")
+# BATCHMAX_LIB selects another build of the same library (the host-sanitizer
+# build of build.py --sanitize, for CPU tests); the default is the in-tree one
+LIB_PATH = os.environ.get("BATCHMAX_LIB") or os.path.join(HERE, "libbatchmax.so")
 
 BM_OK, BM_ERR_INVALID_ARG, BM_ERR_UNSUPPORTED, BM_ERR_CAPACITY, BM_ERR_ORDER, BM_ERR_HIP = range(6)
 BM_F32, BM_BF16 = 0, 1

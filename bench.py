@@ -103,43 +103,62 @@ def hbm_probe():
 
 def peak_probe():
     """What the box achieves against the published peaks: the device's compute
-    units, a large bf16 GEMM through the vendor BLAS (matrix cores), and a plain
-    device copy (HBM).  Context for the roofline fractions, not a target."""
+    units; the library's own probes (bm_probe.h) -- a streaming read of 4 GiB
+    (plain and non-temporal loads) and a loop of independent bf16 MFMAs with no
+    memory traffic; a large bf16 GEMM through the vendor BLAS and a plain
+    device copy.  Context for the roofline fractions, not a target."""
     import torch
 
+    from paper_2412_05693_amd import batchmax as bmx
+
     dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
     props = torch.cuda.get_device_properties(dev)
-    out = {"device": props.name, "compute_units": props.multi_processor_count,
-           "memory_bytes": props.total_memory}
+    cus = props.multi_processor_count
+    out = {"device": props.name, "compute_units": cus, "memory_bytes": props.total_memory}
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3     # seconds per call
+
+    nbytes = 4 << 30
+    buf = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    blocks_r = cus * 16
+    sink = torch.empty(blocks_r * 4, dtype=torch.int32, device=dev)
+    for nt in (False, True):
+        t = timed(lambda: bmx.bm_probe_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), blocks_r,
+                                                   nt, stream.cuda_stream), 10)
+        out["stream_read_nt_gb_per_s" if nt else "stream_read_gb_per_s"] = nbytes / t / 1e9
+    del buf
+    for waves_per_cu in (8, 16):
+        blocks_m, iters = cus * waves_per_cu // 4, 20000
+        fsink = torch.empty(blocks_m * 4, dtype=torch.float32, device=dev)
+        t = timed(lambda: bmx.bm_probe_mfma(iters, fsink.data_ptr(), blocks_m, stream.cuda_stream), 5)
+        flops = blocks_m * 4 * iters * 4 * 32768
+        out[f"mfma_loop_tflops_{waves_per_cu}_waves_per_cu"] = flops / t / 1e12
     n = 8192
     a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
     b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
     c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
-    for _ in range(3):
-        torch.matmul(a, b, out=c)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 20
-    e0.record()
-    for _ in range(reps):
-        torch.matmul(a, b, out=c)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    out["bf16_gemm_tflops"] = 2 * n ** 3 / (ms * 1e-3) / 1e12
+    t = timed(lambda: torch.matmul(a, b, out=c), 20)
+    out["bf16_gemm_tflops"] = 2 * n ** 3 / t / 1e12
     x = torch.ones(HBM_PROBE_BYTES, dtype=torch.uint8, device=dev)
     y = torch.empty_like(x)
-    y.copy_(x)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(reps):
-        y.copy_(x)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    out["copy_gb_per_s"] = 2 * HBM_PROBE_BYTES / (ms * 1e-3) / 1e9     # read + write
-    out["bf16_gemm_frac_of_peak"] = out["bf16_gemm_tflops"] / (PEAK_BF16_MFMA / 1e12)
-    out["copy_frac_of_peak"] = out["copy_gb_per_s"] / (PEAK_HBM / 1e9)
+    t = timed(lambda: y.copy_(x), 20)
+    out["copy_gb_per_s"] = 2 * HBM_PROBE_BYTES / t / 1e9     # read + write
+    for k in list(out):
+        if k.endswith("_tflops") or "tflops_" in k:
+            out[k + "_frac_of_peak"] = out[k] / (PEAK_BF16_MFMA / 1e12)
+        elif k.endswith("_gb_per_s"):
+            out[k + "_frac_of_peak"] = out[k] / (PEAK_HBM / 1e9)
     print(json.dumps({"peak_probe": out}), flush=True)
 
 

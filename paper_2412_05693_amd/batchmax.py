@@ -97,6 +97,8 @@ def _load() -> ctypes.CDLL:
         "bm_destroy": (None, [P]),
         "bm_synth_qkv": (ctypes.c_int, [ctypes.POINTER(bm_synth), I32, I32, P, P, P, I32, P]),
         "bm_philox4x32_10": (ctypes.c_int, [P, P, ctypes.c_int64, P]),
+        "bm_probe_stream_read": (ctypes.c_int, [P, SZ, P, I32, I32, P]),
+        "bm_probe_mfma": (ctypes.c_int, [I32, P, I32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -113,7 +115,7 @@ EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_b
             "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
             "bm_set_score_accumulation", "bm_set_left_padding", "bm_set_split_event",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
-            "bm_philox4x32_10")
+            "bm_philox4x32_10", "bm_probe_stream_read", "bm_probe_mfma")
 
 
 def _check(status: int) -> None:
@@ -230,6 +232,15 @@ def bm_synth_qkv(params: bm_synth, t0: int, n_rows: int, q: int, k: int, v: int,
 
 def bm_philox4x32_10(inp: int, out: int, n: int, stream: int) -> None:
     _check(_lib.bm_philox4x32_10(inp, out, n, stream))
+
+
+def bm_probe_stream_read(src: int, nbytes: int, sink: int, blocks: int, nontemporal: bool,
+                         stream: int) -> None:
+    _check(_lib.bm_probe_stream_read(src, nbytes, sink, blocks, 1 if nontemporal else 0, stream))
+
+
+def bm_probe_mfma(iters: int, sink: int, blocks: int, stream: int) -> None:
+    _check(_lib.bm_probe_mfma(iters, sink, blocks, stream))
 
 
 def make_dims(*, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim, dtype,

@@ -27,7 +27,7 @@ BUILD = os.path.join(HERE, "_build")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libbatchmax.so")
 SOURCES = ["bm_abi.hip", "k_prefill.hip", "k_evict.hip", "k_decode.hip", "k_decode_long.hip",
-           "k_synth.hip"]
+           "k_synth.hip", "k_probe.hip"]
 ARCH = "gfx950"
 
 

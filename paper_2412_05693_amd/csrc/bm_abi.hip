@@ -691,6 +691,27 @@ BM_EXPORT int bm_philox4x32_10(const uint32_t* in, uint32_t* out, int64_t n, hip
 }
 
 // ---------------------------------------------------------------------------
+// roofline probes (bm_probe.h)
+// ---------------------------------------------------------------------------
+BM_EXPORT int bm_probe_stream_read(const void* src, size_t bytes, uint32_t* sink, int32_t blocks,
+                                   int32_t nontemporal, hipStream_t stream) {
+  if (!src || !sink || blocks < 1) return fail(BM_ERR_INVALID_ARG, "null pointer or blocks < 1");
+  if (((uintptr_t)src & 15) || (bytes & 15) || bytes == 0)
+    return fail(BM_ERR_INVALID_ARG, "src and bytes must be 16-byte multiples");
+  const hipError_t e = bm::launch_probe_read(src, bytes, sink, blocks, nontemporal != 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "probe launch");
+  return ok();
+}
+
+BM_EXPORT int bm_probe_mfma(int32_t iters, float* sink, int32_t blocks, hipStream_t stream) {
+  if (!sink || blocks < 1 || iters < 1)
+    return fail(BM_ERR_INVALID_ARG, "null sink, blocks < 1 or iters < 1");
+  const hipError_t e = bm::launch_probe_mfma(iters, sink, blocks, stream);
+  if (e != hipSuccess) return hip_fail(e, "probe launch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
 // cache reset: a fill kernel rather than hipMemsetAsync, so the enqueued work
 // is safe to record into a HIP graph
 // ---------------------------------------------------------------------------

@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "batchmax.h"
+#include "bm_probe.h"
 #include "bm_synth.h"
 
 namespace bm {
@@ -150,5 +151,8 @@ hipError_t launch_reset(float* score, int32_t* len, size_t n_score, size_t n_len
                         hipStream_t stream);
 hipError_t launch_synth_qkv(const SynthArgs& a, hipStream_t stream);
 hipError_t launch_philox(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t stream);
+hipError_t launch_probe_read(const void* src, size_t bytes, uint32_t* sink, int blocks, bool nt,
+                             hipStream_t stream);
+hipError_t launch_probe_mfma(int iters, float* sink, int blocks, hipStream_t stream);
 
 }  // namespace bm

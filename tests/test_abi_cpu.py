@@ -356,3 +356,14 @@ def test_static_workspace_refuses_oversized_dims_before_device_work():
     assert "static workspace" in bmx.bm_last_error()
     assert status_of(bmx.bm_init_static_workspace, dims(b=0), fake_cache(d), 0) == \
         bmx.BM_ERR_INVALID_ARG
+
+
+def test_probe_argument_errors():
+    P = FAKE
+    assert status_of(bmx.bm_probe_stream_read, 0, 1024, P, 4, False, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_probe_stream_read, P + 8, 1024, P, 4, False, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_probe_stream_read, P, 1000, P, 4, False, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_probe_stream_read, P, 1024, P, 0, False, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_probe_mfma, 0, P, 4, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_probe_mfma, 10, 0, 4, 0) == bmx.BM_ERR_INVALID_ARG
+    assert status_of(bmx.bm_probe_mfma, 10, P, 0, 0) == bmx.BM_ERR_INVALID_ARG

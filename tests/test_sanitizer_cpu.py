@@ -29,9 +29,21 @@ print("sanitized library loaded")
 """
 
 
-def _san_env():
+def _stale() -> bool:
+    """The instrumented library is missing or older than a source file."""
     if not os.path.exists(B.LIB_SAN):
-        pytest.skip("sanitizer build missing: python -m paper_2412_05693_amd.build --sanitize")
+        return True
+    built = os.path.getmtime(B.LIB_SAN)
+    for d in (B.CSRC, B.INCLUDE):
+        for f in os.listdir(d):
+            if os.path.getmtime(os.path.join(d, f)) > built:
+                return True
+    return False
+
+
+def _san_env():
+    if _stale():
+        B.build(sanitize=True)
     return B.sanitizer_env()
 
 

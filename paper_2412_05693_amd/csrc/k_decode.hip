@@ -13,7 +13,11 @@
 //      key of the chosen rule (by default ave = score / (pos_now + 1 - pos))
 //      packed with pos into 64 bits, and a workgroup argmin (older entry first
 //      on an exact tie);
-//   4. o_g = sum_j P[g][j] v_j on VALU, V rows read once, 16 bytes per lane;
+//   4. o_g = sum_j P[g][j] v_j on VALU, V rows read once, 16 bytes per lane
+//      (marked non-temporal when the launch's cached K and V exceed the
+//      device's last-level cache: they are not read again before the next
+//      step has streamed the whole cache through; below that size the next
+//      step finds them in the cache);
 //   5. write back the scores; if the cache exceeds kv_max, the new pair takes
 //      the slot of the removed entry (or is dropped if it is the one removed);
 //      otherwise it is appended at slot len.
@@ -36,7 +40,16 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int off) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-template <bool BF16, int D, int G>
+template <bool NT>
+__device__ __forceinline__ u32x4 load_v(const void* p) {
+  if constexpr (NT) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  } else {
+    return *reinterpret_cast<const u32x4*>(p);
+  }
+}
+
+template <bool BF16, int D, int G, bool NTV>
 __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   using E = typename std::conditional<BF16, uint16_t, float>::type;
   constexpr int EPC = 16 / sizeof(E);       // elements per 16-byte chunk
@@ -142,7 +155,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   for (int r = 0; r < UNR; ++r) {
     const int j = kl4 + r * NKL4;
     const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
-    vw[r] = src ? *reinterpret_cast<const u32x4*>(src + c4 * EPC) : u32x4{0, 0, 0, 0};
+    vw[r] = src ? load_v<NTV>(src + c4 * EPC) : u32x4{0, 0, 0, 0};
   }
 
   // ---------------- 2. softmax per query head ----------------
@@ -222,7 +235,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       for (int r = 0; r < UNR; ++r) {
         const int j = j0 + (UNR + r) * NKL;
         const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
-        vn[r] = src ? *reinterpret_cast<const u32x4*>(src + c * EPC) : u32x4{0, 0, 0, 0};
+        vn[r] = src ? load_v<NTV>(src + c * EPC) : u32x4{0, 0, 0, 0};
       }
 #pragma unroll
       for (int r = 0; r < UNR; ++r) {
@@ -323,13 +336,21 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   if (tid == 0) a.len[u] = evict ? len0 : len0 + 1;
 }
 
+// MI355X's last-level (Infinity) cache: 256 MiB
+constexpr size_t kLastLevelCacheBytes = (size_t)256 << 20;
+
 template <bool BF16, int D, int G>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   const int L = a.len0 + 1;
   const int Lp = (L + 3) & ~3;
   const size_t lds = sizeof(float) * ((size_t)G * Lp + Lp + 4 * G * D + Lp);
-  hipLaunchKernelGGL((decode_kernel<BF16, D, G>), dim3((unsigned)a.units), dim3(256), lds, stream,
-                     a);
+  const size_t kv_bytes = (size_t)a.units * 2 * a.len0 * D * (BF16 ? 2 : 4);
+  if (kv_bytes > kLastLevelCacheBytes)
+    hipLaunchKernelGGL((decode_kernel<BF16, D, G, true>), dim3((unsigned)a.units), dim3(256), lds,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<BF16, D, G, false>), dim3((unsigned)a.units), dim3(256), lds,
+                       stream, a);
   return hipGetLastError();
 }
 

@@ -231,11 +231,13 @@ def stack_params(wl: synth.Workload, layer: int, b: int):
 
 
 def run_stack_parity(wl: synth.Workload, checked, *, device="cuda", decode_steps=None,
-                     stop_on_failure=True) -> Stats:
+                     stop_on_failure=True, fused_cut=False) -> Stats:
     """The layer stack: every layer's inputs come from the device generator one
     block (or decode row) at a time; the checked units ``(layer, sample,
     kv_head)`` are compared with the oracle fed by the host evaluation of the
-    same counter-based stream."""
+    same counter-based stream.  ``fused_cut`` runs each block and its cut as
+    one call (the benchmark's path; the state between the two is then not
+    observed)."""
     from paper_2412_05693_amd.batchmax import PDStack, synth_qkv
 
     st = Stats()
@@ -276,9 +278,17 @@ def run_stack_parity(wl: synth.Workload, checked, *, device="cuda", decode_steps
         for layer in range(wl.n_layers):
             pd = stack.layers[layer]
             synth_qkv(params[layer], t0, q, k, v)
-            pd.prefill_block(t0, n, q, k, v, o, row=0)
             units = by_layer.get(layer)
-            if units:
+            if fused_cut:
+                pd.prefill_block_cut(t0, n, q, k, v, o, row=0)
+                for (bi, hk) in units or ():
+                    u = (layer, bi, hk)
+                    uq, uk, uv = uin[u]
+                    ref = orcs[u].prefill_block(t0, uq[:, t0:t0 + n], uk[t0:t0 + n], uv[t0:t0 + n])
+                    check_out(f"block {t0}", o, u, n, ref)
+            else:
+                pd.prefill_block(t0, n, q, k, v, o, row=0)
+            if units and not fused_cut:
                 length = pd.length
                 pos, score, dlen = _snapshot(pd, units, length)
                 for i, (bi, hk) in enumerate(units):
@@ -288,7 +298,8 @@ def run_stack_parity(wl: synth.Workload, checked, *, device="cuda", decode_steps
                     check_out(f"block {t0}", o, u, n, ref)
                     _compare_state(f"block {t0} unit {u}", orcs[u], pos[i], score[i], dlen[i],
                                    length, st)
-            pd.evict_compact(t0 + n - 1)
+            if not fused_cut:
+                pd.evict_compact(t0 + n - 1)
             if units:
                 length = pd.length
                 pos, score, dlen = _snapshot(pd, units, length)

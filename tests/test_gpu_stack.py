@@ -74,7 +74,8 @@ def test_synth_qkv_device_matches_host(dtype, d, G, t0, rows):
             assert np.array_equal(gq[bi, hk * G:(hk + 1) * G], uq[:, t0:t0 + rows])
 
 
-def test_c5_stack_parity_reduced_batch():
+@pytest.mark.parametrize("fused_cut", [False, True])
+def test_c5_stack_parity_reduced_batch(fused_cut):
     _need_gpu()
     from pd_harness import run_stack_parity
 
@@ -86,8 +87,8 @@ def test_c5_stack_parity_reduced_batch():
                (L - 1, 0, 5), (L - 1, 1, 0), (L - 1, 0, 7), (L - 1, 1, 3), (L - 2, 0, 4),
                (L - 2, 1, 6), (L // 4, 1, 1)]
     _say(f"[stack] {wl.name} b={wl.b} layers={L} s={wl.s} kv={wl.kv_max} B={wl.block} "
-         f"D={wl.n_decode} units={checked}")
-    st = run_stack_parity(wl, checked)
+         f"D={wl.n_decode} fused_cut={fused_cut} units={checked}")
+    st = run_stack_parity(wl, checked, fused_cut=fused_cut)
     _say(f"[stack] -> {st.summary()}")
     assert not st.failures, "\n".join(st.failures)
     assert st.cuts == len(checked) * (wl.s // wl.block - wl.kv_max // wl.block + wl.n_decode)
@@ -95,8 +96,10 @@ def test_c5_stack_parity_reduced_batch():
 
 def test_c5_stack_parity_full_batch():
     """The 32-layer stack at the batch the benchmark runs (the largest that fits
-    the device), checked on sampled units of the first, middle and last layers
-    and of the first, middle and last samples."""
+    the device) and on its path (each block and its cut in one call: attention,
+    then the fused fold/select/compaction kernel), checked on sampled units of
+    the first, middle and last layers and of the first, middle and last
+    samples."""
     _need_gpu()
     import gc
 
@@ -116,8 +119,8 @@ def test_c5_stack_parity_full_batch():
     L = wl.n_layers
     checked = [(0, 0, 0), (0, b - 1, 7), (L // 2, b // 2, 3), (L // 2, b - 1, 4),
                (L - 1, 0, 5), (L - 1, b - 1, 2)]
-    _say(f"[stack] {wl.name} full batch b={b} layers={L} s={wl.s} units={checked}")
-    st = run_stack_parity(wl, checked)
+    _say(f"[stack] {wl.name} full batch b={b} layers={L} s={wl.s} fused_cut=True units={checked}")
+    st = run_stack_parity(wl, checked, fused_cut=True)
     _say(f"[stack] -> {st.summary()}")
     assert not st.failures, "\n".join(st.failures)
     assert st.cuts == len(checked) * (wl.s // wl.block - wl.kv_max // wl.block + wl.n_decode)

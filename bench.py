@@ -436,12 +436,19 @@ def gpu_bench(name, overrides, steps, warmup, method="bm", graph=False, fused_cu
     }
 
 
+FUSED_CUT_MAX_ENTRIES = 4096   # bm_prefill_block_cut's one-workgroup cut (include/batchmax.h)
+
+
 def cut_fixed_bytes(wl, b) -> int:
-    """HBM bytes of one prefill step's fused fold/cut launches that do not
-    depend on the data: every live slot's partial column sums (one row per
-    attention workgroup that saw the slot), its score read and written and its
-    position read.  The moved K/V rows come on top (their number depends on
-    which entries the rule removes)."""
+    """HBM bytes of one prefill step's cut launches that do not depend on the
+    data.  Up to 4096 live entries one fold/cut kernel per block reads every
+    live slot's partial column sums (one row per attention workgroup that saw
+    the slot, and only when scores accumulate), reads and writes its score,
+    reads its position, and under TOVA its last-query weight.  Above 4096 the
+    call folds with the score-reduce kernel (cached scores read, every score
+    written, the partials) and, if the block overflows the bound, cuts with
+    the select kernel (scores and positions read).  The moved K/V rows come on
+    top (their number depends on which entries the rule removes)."""
     from paper_2412_05693_amd import batchmax as bmx
 
     ppw = bmx.bm_prefill_positions_per_workgroup(bmx.make_dims(
@@ -452,9 +459,12 @@ def cut_fixed_bytes(wl, b) -> int:
     for t0 in range(0, wl.s, wl.block):
         n = min(wl.block, wl.s - t0)
         npt = -(-n // ppw)
-        part = length * npt + sum(npt - r // ppw for r in range(n))
+        part = length * npt + sum(npt - r // ppw for r in range(n)) if wl.accumulate else 0
         live = length + n
-        total += 4 * part + 12 * live
+        if live <= FUSED_CUT_MAX_ENTRIES:
+            total += 4 * part + 12 * live + (4 * live if wl.rule == "tova" else 0)
+        else:
+            total += 4 * part + 4 * length + 4 * live + (8 * live if live > wl.kv_max else 0)
         length = min(wl.kv_max, live)
     return total * b * wl.n_kv_heads
 
@@ -463,7 +473,7 @@ def cut_roofline(nbytes, ms):
     gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
     return {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
             "frac": gbs / (PEAK_HBM / 1e9), "algorithmic_bytes_per_step": nbytes,
-            "algorithmic_basis": "partial sums, scores and positions only (moved rows excluded)"}
+            "algorithmic_basis": "partial sums (when scores accumulate), scores and positions only (moved rows excluded)"}
 
 
 STACK_RESERVE = 3 << 30      # device bytes left to the runtime when planning the batch

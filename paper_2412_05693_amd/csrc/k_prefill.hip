@@ -254,26 +254,47 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   const Geo s = make_geo<G, PAD>(a);
   const int tid = threadIdx.x;
 
+  constexpr int PT = kWaves * kRowsPerWave / G;   // block positions per workgroup
+
   // ---- append the workgroup's block rows to the cache tail (Sec. 3.2: new
-  //      entries start with score 0; the score is written by score_reduce) ----
+  //      entries start with score 0; the score is written by score_reduce).
+  //      The loads are issued here, with the query loads and the first tile
+  //      copies behind them, and the stores follow the wait those need anyway,
+  //      so the workgroup waits for memory once before its first tile. ----
   const int64_t plane = ((int64_t)s.bi * a.n_kv_heads + s.hk) * a.seq_ld;
+  constexpr int NA = (PT * C::CPR + kThreads - 1) / kThreads;   // chunks per thread
+  const int app_chunks = (s.in_rows - s.pbase) * C::CPR;
+  u32x4 app_k[NA], app_v[NA];
   {
-    constexpr int CPR = C::CPR;
-    const int r0 = s.pbase, r1 = s.in_rows;
     const E* kin = static_cast<const E*>(a.kin);
     const E* vin = static_cast<const E*>(a.vin);
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int c = tid + i * kThreads;
+      if (c < app_chunks) {
+        const int r = s.pbase + c / C::CPR, cc = c % C::CPR;
+        const int64_t src = (plane + r) * D + cc * (16 / sizeof(E));
+        app_k[i] = *reinterpret_cast<const u32x4*>(kin + src);
+        app_v[i] = *reinterpret_cast<const u32x4*>(vin + src);
+      }
+    }
+  }
+  auto append_store = [&]() __device__ {
     E* kc = static_cast<E*>(a.kc);
     E* vc = static_cast<E*>(a.vc);
-    for (int c = tid; c < (r1 - r0) * CPR; c += kThreads) {
-      const int r = r0 + c / CPR, cc = c % CPR;
-      const int64_t dst = ((int64_t)s.u * a.cap + a.len0 + r) * D + cc * (16 / sizeof(E));
-      const int64_t src = (plane + r) * D + cc * (16 / sizeof(E));
-      *reinterpret_cast<u32x4*>(kc + dst) = *reinterpret_cast<const u32x4*>(kin + src);
-      *reinterpret_cast<u32x4*>(vc + dst) = *reinterpret_cast<const u32x4*>(vin + src);
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int c = tid + i * kThreads;
+      if (c < app_chunks) {
+        const int r = s.pbase + c / C::CPR, cc = c % C::CPR;
+        const int64_t dst = ((int64_t)s.u * a.cap + a.len0 + r) * D + cc * (16 / sizeof(E));
+        *reinterpret_cast<u32x4*>(kc + dst) = app_k[i];
+        *reinterpret_cast<u32x4*>(vc + dst) = app_v[i];
+      }
     }
-    for (int r = r0 + tid; r < r1; r += kThreads)
+    for (int r = s.pbase + tid; r < s.in_rows; r += kThreads)
       a.pos[(int64_t)s.u * a.cap + a.len0 + r] = a.t0 + r;
-  }
+  };
 
   // ---- row sources of the tiles (out-of-range rows read as zero) ----
   const uint64_t kc_base = (uint64_t)(static_cast<const E*>(a.kc) + (int64_t)s.u * a.cap * D);
@@ -495,10 +516,15 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   dma_v(vb0, tile_info(a, s, 0));
   if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  append_store();
   __syncthreads();
   // logits ping-pong between two register sets; the loop is unrolled by two so
   // every buffer choice below is a compile-time constant
   f32x16 sa[2], sb[2];
+  // sweep 2's first K tiles are fetched during sweep 1's last iteration (not
+  // with left padding: that iteration still reads the position ring slots the
+  // early copies would refill)
+  const bool early_k2 = !PAD && a.accumulate;
   if (tile_active(s, tile_info(a, s, 0))) qk_st(kb0, sa);
   __syncthreads();   // every wave has read K(0) before iteration 0 refills its buffer
   // iteration t (parity P = t & 1): K(t+1) and V(t) are in LDS and `cur` holds
@@ -516,6 +542,12 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       const TileInfo tn = tile_info(a, s, t + 1);
       dma_v(v_fill, tn);
       if (tile_active(s, tn)) qk_st(k_next, nxt);
+    }
+    if (early_k2 && t == nt - 1) {
+      // both K buffers are free in the last iteration: fetch the first two K
+      // tiles of sweep 2 now, so they land with this iteration's wait
+      dma_k(kb0, tile_info(a, s, 0), 0);
+      if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
     }
     if (tile_active(s, ti)) {
       if constexpr (PAD) {
@@ -575,7 +607,6 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   // TOVA: the workgroup holding the block's last row also keeps that row's
   // weights (summed over the heads) for every key; its waves for that row find
   // it in accumulator register ri of lane half hr
-  constexpr int PT = kWaves * kRowsPerWave / G;
   const int last_row = a.n_tok - 1;
   const bool wg_last = a.lastw && s.pbase <= last_row && last_row < s.pbase + PT;
   const bool wave_last = wg_last && s.wrow0 <= last_row && last_row < s.wrow0 + kRowsPerWave;
@@ -606,11 +637,14 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     }
   };
 
-  // prologue: K(0), K(1) land in LDS; logits of tile 0
-  dma_k(kb0, tile_info(a, s, 0), 0);
-  if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
-  __builtin_amdgcn_s_waitcnt(kWaitVm0);
-  __syncthreads();
+  // prologue: K(0), K(1) land in LDS (already there when sweep 1's last
+  // iteration fetched them); logits of tile 0
+  if (!early_k2) {
+    dma_k(kb0, tile_info(a, s, 0), 0);
+    if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    __syncthreads();
+  }
   if (tile_active(s, tile_info(a, s, 0))) qk_s(kb0, sa);
   __syncthreads();   // every wave has read K(0) before iteration 0 refills its buffer
   // iteration t (parity P = t & 1): K(t+1) is in LDS and `cur` holds tile t's logits

@@ -142,3 +142,23 @@ def test_cut_fixed_bytes():
     b1 = 256 * npt + b0
     want = (4 * b0 + 12 * 256) + (4 * b1 + 12 * 512)
     assert bench.cut_fixed_bytes(wl, 1) == want * wl.n_kv_heads
+
+
+def test_cut_fixed_bytes_without_accumulation_tova_and_long_caches():
+    """No partial sums when scores do not accumulate (the comparators); the
+    last-query weight under TOVA; above 4096 live entries the score-reduce fold
+    (cached scores read, every score written) with no position reads."""
+    wl = synth.WORKLOADS["c2"].with_(b=1, s=512, kv_max=256, block=256)
+    d = bmx.make_dims(b=1, s=512, kv_max=256, block=256, max_gen=wl.n_decode, n_heads=32,
+                      n_kv_heads=8, head_dim=128, dtype="bf16")
+    ppw = bmx.bm_prefill_positions_per_workgroup(d)
+    npt = 256 // ppw
+    b0 = sum(npt - r // ppw for r in range(256))
+    b1 = 256 * npt + b0
+    assert bench.cut_fixed_bytes(wl.with_(accumulate=False), 1) == (12 * 256 + 12 * 512) * 8
+    want_tova = (4 * b0 + 16 * 256) + (4 * b1 + 16 * 512)
+    assert bench.cut_fixed_bytes(wl.with_(rule="tova"), 1) == want_tova * 8
+    # a full-cache prompt of 8192 tokens in blocks of 4096: the second block
+    # holds 8192 live entries, past the fused cut's 4096
+    big = synth.WORKLOADS["c2"].with_(b=1, s=8192, kv_max=8192, block=4096, accumulate=False)
+    assert bench.cut_fixed_bytes(big, 1) == (12 * 4096 + (4 * 4096 + 4 * 8192)) * 8

@@ -109,13 +109,15 @@ __device__ __forceinline__ f32x16 mfma_step(typename Cfg<BF16, D>::qfrag_t a,
   }
 }
 
-// fragment of LDS row `row` of a K tile for K-step kk, lane half h
+// fragment of LDS row `row` of a K tile for K-step kk, lane half h.  bf16:
+// K-step kk contracts the 16-byte chunks 2 kk (lane half 0) and 2 kk + 1 (lane
+// half 1) of d, so the two halves of a query row's load fall in one cache line
 template <bool BF16, int D>
 __device__ __forceinline__ typename Cfg<BF16, D>::qfrag_t k_frag(const char* ks, int row, int h,
                                                                  int kk) {
   using C = Cfg<BF16, D>;
   if constexpr (BF16) {
-    const int b = (h * (D / 2) + 8 * kk) * 2;
+    const int b = (2 * kk + h) * 16;
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + row * C::KSTRIDE + b));
   } else {
     const int b = (h * (D / 2) + kk) * 4;
@@ -336,19 +338,21 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     dma_rows<BF16, D, false>(dst, tile_src(ti, false), ti, s);
   };
 
-  // ---- query fragments: lane (n, h) holds row n, d-range [h*D/2, (h+1)*D/2) ----
+  // ---- query fragments: lane (n, h) holds row n; bf16: the d-chunks 2 kk + h
+  //      (the order k_frag reads K in), fp32: d-range [h*D/2, (h+1)*D/2) ----
   typename C::qfrag_t qf[C::QSTEPS];
   {
     const int qh = s.hk * G + s.g;
     const E* q = static_cast<const E*>(a.q) +
-                 (((int64_t)s.bi * a.n_heads + qh) * a.seq_ld + s.row) * D + s.h * (D / 2);
+                 (((int64_t)s.bi * a.n_heads + qh) * a.seq_ld + s.row) * D;
 #pragma unroll
     for (int kk = 0; kk < C::QSTEPS; ++kk) {
       if constexpr (BF16) {
-        const u32x4 w = s.qvalid ? *reinterpret_cast<const u32x4*>(q + 8 * kk) : u32x4{0, 0, 0, 0};
+        const u32x4 w = s.qvalid ? *reinterpret_cast<const u32x4*>(q + 8 * (2 * kk + s.h))
+                                 : u32x4{0, 0, 0, 0};
         qf[kk] = __builtin_bit_cast(bf16x8, w);
       } else {
-        qf[kk] = s.qvalid ? q[kk] : 0.0f;
+        qf[kk] = s.qvalid ? q[s.h * (D / 2) + kk] : 0.0f;
       }
     }
   }
@@ -574,8 +578,11 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     const float inv = 1.0f / l_tot;
     lse2 = s.qvalid && !s.qpad ? m_run + __builtin_amdgcn_logf(l_tot) : kPosInf;
     if (s.qvalid) {
-      const int qh = s.hk * G + s.g;
-      E* o = static_cast<E*>(a.o) + (((int64_t)s.bi * a.n_heads + qh) * a.seq_ld + s.row) * D;
+      // the output row's address is computed again here rather than kept from
+      // the query load (which would hold two registers through both sweeps)
+      int orow = s.row, ohead = s.bi * a.n_heads + s.hk * G + s.g;
+      asm volatile("" : "+v"(orow), "+v"(ohead));
+      E* o = static_cast<E*>(a.o) + ((int64_t)ohead * a.seq_ld + orow) * D;
 #pragma unroll
       for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll

@@ -577,9 +577,42 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   if (s.wave_active) {
     const float inv = 1.0f / l_tot;
     lse2 = s.qvalid && !s.qpad ? m_run + __builtin_amdgcn_logf(l_tot) : kPosInf;
-    if (s.qvalid) {
-      // the output row's address is computed again here rather than kept from
-      // the query load (which would hold two registers through both sweeps)
+    // a pad row has no output (zeros)
+    const float sc = s.qpad ? 0.0f : inv;
+    if constexpr (BF16) {
+      // The wave's 32 output rows are contiguous in memory (one head, 32
+      // consecutive positions).  They go through LDS -- the V buffers are
+      // idle once sweep 1 is over; each wave uses its own padded 32-row
+      // region -- so the stores are whole 1 KB runs instead of 16 bytes per
+      // row per instruction.
+      constexpr int OSTRIDE = C::KSTRIDE;   // padded row: D * 2 + 16 bytes
+      static_assert(kWaves == 4 && 2 * kRowsPerWave * OSTRIDE <= C::V_BYTES,
+                    "two waves' rows per V buffer");
+      char* ost = (s.w < 2 ? vb0 : vb1) + (s.w & 1) * (kRowsPerWave * OSTRIDE);
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d0 = 32 * mt + 8 * i + 4 * s.h;
+          const u32x2 w = {pack_bf16x2(oacc[mt][4 * i + 0] * sc, oacc[mt][4 * i + 1] * sc),
+                           pack_bf16x2(oacc[mt][4 * i + 2] * sc, oacc[mt][4 * i + 3] * sc)};
+          *reinterpret_cast<u32x2*>(ost + s.n * OSTRIDE + d0 * 2) = w;
+        }
+      // the output row's address is computed here rather than kept from the
+      // query load (which would hold two registers through both sweeps)
+      int orow0 = s.wrow0, ohead = s.bi * a.n_heads + s.hk * G + s.g;
+      asm volatile("" : "+v"(orow0), "+v"(ohead));
+      char* o = reinterpret_cast<char*>(static_cast<E*>(a.o) + ((int64_t)ohead * a.seq_ld + orow0) * D);
+      constexpr int RUNS = kRowsPerWave * RB / 1024;   // 1 KB runs per wave
+      constexpr int RPR = 1024 / RB;                   // rows per run
+#pragma unroll
+      for (int j = 0; j < RUNS; ++j) {
+        const int r = RPR * j + s.lane / (RB / 16), c = s.lane % (RB / 16);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(ost + r * OSTRIDE + c * 16);
+        if (s.wrow0 + r < a.n_tok)
+          *reinterpret_cast<u32x4*>(o + (int64_t)r * RB + c * 16) = v;
+      }
+    } else if (s.qvalid) {
       int orow = s.row, ohead = s.bi * a.n_heads + s.hk * G + s.g;
       asm volatile("" : "+v"(orow), "+v"(ohead));
       E* o = static_cast<E*>(a.o) + ((int64_t)ohead * a.seq_ld + orow) * D;
@@ -588,16 +621,9 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int d0 = 32 * mt + 8 * i + 4 * s.h;
-          // a pad row has no output (zeros)
-          const float sc = s.qpad ? 0.0f : inv;
           const float x0 = oacc[mt][4 * i + 0] * sc, x1 = oacc[mt][4 * i + 1] * sc;
           const float x2 = oacc[mt][4 * i + 2] * sc, x3 = oacc[mt][4 * i + 3] * sc;
-          if constexpr (BF16) {
-            u32x2 w = {pack_bf16x2(x0, x1), pack_bf16x2(x2, x3)};
-            *reinterpret_cast<u32x2*>(o + d0) = w;
-          } else {
-            *reinterpret_cast<float4*>(o + d0) = make_float4(x0, x1, x2, x3);
-          }
+          *reinterpret_cast<float4*>(o + d0) = make_float4(x0, x1, x2, x3);
         }
     }
   }

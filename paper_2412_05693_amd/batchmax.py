@@ -99,6 +99,7 @@ def _load() -> ctypes.CDLL:
         "bm_philox4x32_10": (ctypes.c_int, [P, P, ctypes.c_int64, P]),
         "bm_probe_stream_read": (ctypes.c_int, [P, SZ, P, I32, I32, P]),
         "bm_probe_mfma": (ctypes.c_int, [I32, P, I32, P]),
+        "bm_prefill_timeline": (ctypes.c_int, [P, I32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -115,7 +116,8 @@ EXPORTED = ("bm_abi_version", "bm_last_error", "bm_cache_slots", "bm_workspace_b
             "bm_set_decode_removal", "bm_set_rank_rule", "bm_set_decode_bound",
             "bm_set_score_accumulation", "bm_set_left_padding", "bm_set_split_event",
             "bm_decode_step", "bm_ctx_len", "bm_ctx_next_pos", "bm_destroy", "bm_synth_qkv",
-            "bm_philox4x32_10", "bm_probe_stream_read", "bm_probe_mfma")
+            "bm_philox4x32_10", "bm_probe_stream_read", "bm_probe_mfma",
+            "bm_prefill_timeline")
 
 
 def _check(status: int) -> None:
@@ -241,6 +243,20 @@ def bm_probe_stream_read(src: int, nbytes: int, sink: int, blocks: int, nontempo
 
 def bm_probe_mfma(iters: int, sink: int, blocks: int, stream: int) -> None:
     _check(_lib.bm_probe_mfma(iters, sink, blocks, stream))
+
+
+TIMELINE_FIELDS = 16
+TIMELINE_MAX_RECORDS = 65536
+
+
+def bm_prefill_timeline(n_records: int):
+    """The last prefill launch's per-workgroup timeline records (a library
+    built with BM_PREFILL_TIMELINE): uint64 array [n_records, 16]."""
+    import numpy as np
+
+    out = np.zeros((n_records, TIMELINE_FIELDS), dtype=np.uint64)
+    _check(_lib.bm_prefill_timeline(out.ctypes.data_as(ctypes.c_void_p), n_records))
+    return out
 
 
 def make_dims(*, b, s, kv_max, block, max_gen, n_heads, n_kv_heads, head_dim, dtype,

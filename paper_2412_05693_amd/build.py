@@ -2,9 +2,15 @@
 
     python -m paper_2412_05693_amd.build              # the library
     python -m paper_2412_05693_amd.build --sanitize   # host-side ASan + UBSan build
+    python -m paper_2412_05693_amd.build --timeline   # prefill timestamp build
 
 Every call recompiles.  Objects go to ``paper_2412_05693_amd/_build/``; the
 library lands next to this file, where ``batchmax.py`` loads it.
+
+``--timeline`` builds ``libbatchmax_timeline.so`` with BM_PREFILL_TIMELINE
+defined: its prefill attention kernel records per-workgroup timestamps
+(include/bm_probe.h; read with ``python -m paper_2412_05693_amd.timeline``).
+Measurement only; the ordinary library is compiled without it.
 
 ``--sanitize`` builds ``libbatchmax_san.so`` with AddressSanitizer and
 UndefinedBehaviorSanitizer on the host code only (argument checks, context
@@ -51,6 +57,8 @@ SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=unde
             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
             "-Xarch_host", "-g"]
 LIB_SAN = os.path.join(HERE, "libbatchmax_san.so")
+LIB_TIMELINE = os.path.join(HERE, "libbatchmax_timeline.so")
+TIMELINE = ["-DBM_PREFILL_TIMELINE"]
 
 
 def _compile(src: str, extra=(), tag: str = "") -> str:
@@ -62,9 +70,14 @@ def _compile(src: str, extra=(), tag: str = "") -> str:
     return obj
 
 
-def build(jobs: int = 4, sanitize: bool = False) -> str:
+def build(jobs: int = 4, sanitize: bool = False, timeline: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    extra, tag, lib = (SANITIZE, "_san", LIB_SAN) if sanitize else ((), "", LIB)
+    if sanitize:
+        extra, tag, lib = SANITIZE, "_san", LIB_SAN
+    elif timeline:
+        extra, tag, lib = TIMELINE, "_tl", LIB_TIMELINE
+    else:
+        extra, tag, lib = (), "", LIB
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda src: _compile(src, extra, tag), SOURCES))
     tmp = lib + ".tmp"
@@ -97,5 +110,5 @@ def sanitizer_env() -> dict:
 
 
 if __name__ == "__main__":
-    print(build(sanitize="--sanitize" in sys.argv[1:]))
+    print(build(sanitize="--sanitize" in sys.argv[1:], timeline="--timeline" in sys.argv[1:]))
     sys.exit(0)

@@ -711,6 +711,16 @@ BM_EXPORT int bm_probe_mfma(int32_t iters, float* sink, int32_t blocks, hipStrea
   return ok();
 }
 
+BM_EXPORT int bm_prefill_timeline(uint64_t* dst, int32_t n_records) {
+  if (!bm::timeline_enabled())
+    return fail(BM_ERR_UNSUPPORTED, "this library was built without BM_PREFILL_TIMELINE");
+  if (!dst || n_records < 1 || n_records > BM_TIMELINE_MAX_RECORDS)
+    return fail(BM_ERR_INVALID_ARG, "null dst or n_records outside [1, %d]", BM_TIMELINE_MAX_RECORDS);
+  const hipError_t e = bm::read_timeline(dst, n_records);
+  if (e != hipSuccess) return hip_fail(e, "timeline copy");
+  return ok();
+}
+
 // ---------------------------------------------------------------------------
 // cache reset: a fill kernel rather than hipMemsetAsync, so the enqueued work
 // is safe to record into a HIP graph

@@ -154,5 +154,8 @@ hipError_t launch_philox(const uint32_t* in, uint32_t* out, int64_t n, hipStream
 hipError_t launch_probe_read(const void* src, size_t bytes, uint32_t* sink, int blocks, bool nt,
                              hipStream_t stream);
 hipError_t launch_probe_mfma(int iters, float* sink, int blocks, hipStream_t stream);
+// prefill timeline records (a BM_PREFILL_TIMELINE build; else hipErrorNotSupported)
+bool timeline_enabled();
+hipError_t read_timeline(uint64_t* dst, int n_records);
 
 }  // namespace bm

@@ -55,6 +55,29 @@ constexpr float kRescaleLog2 = 8.0f;
 // s_waitcnt with vmcnt(0) and the other counters left alone
 constexpr int kWaitVm0 = 0x0F70;
 
+// ---- prefill timeline (measurement builds: BM_PREFILL_TIMELINE) ----
+// Thread 0 of each workgroup keeps the fields of include/bm_probe.h in
+// registers and stores them at its end; in the ordinary build every use sits
+// in an `if constexpr (kTimeline)` branch and nothing is emitted.
+#ifdef BM_PREFILL_TIMELINE
+constexpr bool kTimeline = true;
+__device__ uint64_t g_timeline[(size_t)BM_TIMELINE_MAX_RECORDS * BM_TIMELINE_FIELDS];
+__device__ __forceinline__ void timeline_store(int id, const uint64_t* tl) {
+  if (threadIdx.x == 0 && id < BM_TIMELINE_MAX_RECORDS) {
+#pragma unroll
+    for (int i = 0; i < BM_TIMELINE_FIELDS; ++i) g_timeline[(size_t)id * BM_TIMELINE_FIELDS + i] = tl[i];
+  }
+}
+#else
+constexpr bool kTimeline = false;
+__device__ __forceinline__ void timeline_store(int, const uint64_t*) {}
+#endif
+// the constant-rate real-time counter (read only in timeline builds)
+__device__ __forceinline__ uint64_t tl_now() {
+  if constexpr (kTimeline) return __builtin_amdgcn_s_memrealtime();
+  return 0;
+}
+
 __device__ __forceinline__ int kappa(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
@@ -253,8 +276,38 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   // the block's last query's weights per wave (TOVA's key), double-buffered like cs
   __shared__ float lws0[kWaves][kKeyTile];
   __shared__ float lws1[kWaves][kKeyTile];
+  uint64_t tl[BM_TIMELINE_FIELDS] = {};
+  if constexpr (kTimeline) tl[BM_TL_ENTRY] = tl_now();
   const Geo s = make_geo<G, PAD>(a);
   const int tid = threadIdx.x;
+  auto stamp = [&](int field) __device__ {
+    if constexpr (kTimeline) tl[field] = tl_now();
+  };
+  auto timeline_end = [&]() __device__ {
+    if constexpr (kTimeline) {
+      tl[BM_TL_END] = tl_now();
+      // HW_ID (all 32 bits) and, above it, XCC_ID (hardware registers 4 and 20)
+      tl[BM_TL_HW_ID] = (uint64_t)__builtin_amdgcn_s_getreg(0xF804) |
+                        ((uint64_t)__builtin_amdgcn_s_getreg(0xF814) << 32);
+      tl[BM_TL_ITEM] = ((uint64_t)s.u << 32) | (uint32_t)s.pt;
+      tl[BM_TL_TILES] = (uint64_t)s.nt;
+      timeline_store(blockIdx.x, tl);
+    }
+  };
+  // end of a tile: wait for this wave's copies, then for every wave
+  auto wait_and_sync = [&](int f_wait, int f_barrier) __device__ {
+    if constexpr (kTimeline) {
+      const uint64_t a0 = tl_now();
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
+      const uint64_t a1 = tl_now();
+      __syncthreads();
+      tl[f_wait] += a1 - a0;
+      tl[f_barrier] += tl_now() - a1;
+    } else {
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
+      __syncthreads();
+    }
+  };
 
   constexpr int PT = kWaves * kRowsPerWave / G;   // block positions per workgroup
 
@@ -357,6 +410,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     }
   }
 
+  stamp(BM_TL_QUERY_ISSUED);
   const int nt = s.nt;
   const float c2 = a.scale_log2;
   // the row this lane's causal mask uses (padding rows reuse the last real row)
@@ -519,9 +573,11 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   dma_k(kb0, tile_info(a, s, 0), 0);
   dma_v(vb0, tile_info(a, s, 0));
   if (nt > 1) dma_k(kb1, tile_info(a, s, 1), 1);
+  stamp(BM_TL_COPIES_ISSUED);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   append_store();
   __syncthreads();
+  stamp(BM_TL_FIRST_TILE);
   // logits ping-pong between two register sets; the loop is unrolled by two so
   // every buffer choice below is a compile-time constant
   f32x16 sa[2], sb[2];
@@ -541,10 +597,12 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     char* v_fill = P == 0 ? vb1 : vb0;
     const int32_t* pk_cur = pk_ring[t % 3];       // positions of tile t
     const TileInfo ti = tile_info(a, s, t);
+    const uint64_t issue0 = tl_now();
     if (t + 2 < nt) dma_k(k_fill, tile_info(a, s, t + 2), t + 2);
     if (t + 1 < nt) {
       const TileInfo tn = tile_info(a, s, t + 1);
       dma_v(v_fill, tn);
+      if constexpr (kTimeline) tl[BM_TL_S1_COPY_ISSUE] += tl_now() - issue0;
       if (tile_active(s, tn)) qk_st(k_next, nxt);
     }
     if (early_k2 && t == nt - 1) {
@@ -563,13 +621,13 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
       else
         sweep1_tile(std::false_type{}, cur, v_cur, ti);
     }
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
-    __syncthreads();
+    wait_and_sync(BM_TL_S1_WAIT, BM_TL_S1_BARRIER);
   };
   for (int t = 0; t < nt; t += 2) {
     sweep1_iter(std::integral_constant<int, 0>{}, t, sa, sb);
     if (t + 1 < nt) sweep1_iter(std::integral_constant<int, 1>{}, t + 1, sb, sa);
   }
+  stamp(BM_TL_SWEEP1_END);
 
   // ---- finish rows: normalise, store O, row log-sum-exp (log2 units) ----
   const float l_tot = xhalf_sum(l_run);
@@ -630,7 +688,11 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 
   // ======================= sweep 2: exact column sums ========================
   // (skipped when the caller asked for outputs only)
-  if (!a.accumulate) return;
+  stamp(BM_TL_OUTPUT_STORED);
+  if (!a.accumulate) {
+    timeline_end();
+    return;
+  }
   // S orientation: lane (n, h) holds key n of a 32-key sub-tile and rows
   // 8i + 4h + j of the wave's 32 rows in accumulator register 4i + j.
   float lse_r[16];
@@ -680,6 +742,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
   }
   if (tile_active(s, tile_info(a, s, 0))) qk_s(kb0, sa);
   __syncthreads();   // every wave has read K(0) before iteration 0 refills its buffer
+  stamp(BM_TL_SWEEP2_START);
   // iteration t (parity P = t & 1): K(t+1) is in LDS and `cur` holds tile t's logits
   auto sweep2_iter = [&](auto par, int t, f32x16* cur, f32x16* nxt) __device__ {
     constexpr int P = decltype(par)::value;
@@ -732,8 +795,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
         if (s.h == 0) lws[s.w][key] = v;
       }
     }
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
-    __syncthreads();
+    wait_and_sync(BM_TL_S2_WAIT, BM_TL_S2_BARRIER);
     if (tid < ti.valid) {
       float acc = 0.0f;
 #pragma unroll
@@ -751,6 +813,7 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
     sweep2_iter(std::integral_constant<int, 0>{}, t, sa, sb);
     if (t + 1 < nt) sweep2_iter(std::integral_constant<int, 1>{}, t + 1, sb, sa);
   }
+  timeline_end();
 }
 
 // Fold the per-workgroup partial column sums into the scores, in workgroup
@@ -808,6 +871,20 @@ hipError_t launch_prefill(const PrefillArgs& a, int dtype, int head_dim, int gro
     if (head_dim == 64) return launch_g<false, 64>(a, group, stream);
   }
   return hipErrorInvalidValue;
+}
+
+bool timeline_enabled() { return kTimeline; }
+
+hipError_t read_timeline(uint64_t* dst, int n_records) {
+#ifdef BM_PREFILL_TIMELINE
+  return hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_timeline),
+                             (size_t)n_records * BM_TIMELINE_FIELDS * sizeof(uint64_t), 0,
+                             hipMemcpyDeviceToHost);
+#else
+  (void)dst;
+  (void)n_records;
+  return hipErrorNotSupported;
+#endif
 }
 
 hipError_t launch_score_reduce(const PrefillArgs& a, hipStream_t stream) {

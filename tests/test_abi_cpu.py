@@ -367,3 +367,27 @@ def test_probe_argument_errors():
     assert status_of(bmx.bm_probe_mfma, 0, P, 4, 0) == bmx.BM_ERR_INVALID_ARG
     assert status_of(bmx.bm_probe_mfma, 10, 0, 4, 0) == bmx.BM_ERR_INVALID_ARG
     assert status_of(bmx.bm_probe_mfma, 10, P, 0, 0) == bmx.BM_ERR_INVALID_ARG
+
+
+def test_prefill_timeline_only_in_timeline_build():
+    """The ordinary library records no timeline and says so; the timestamp
+    build checks its arguments (neither call touches a GPU)."""
+    import subprocess
+    import sys
+
+    with pytest.raises(bmx.BatchMaxError) as e:
+        bmx.bm_prefill_timeline(4)
+    assert e.value.status == bmx.BM_ERR_UNSUPPORTED
+    tl_lib = os.path.join(ROOT, "paper_2412_05693_amd", "libbatchmax_timeline.so")
+    if not os.path.exists(tl_lib):
+        pytest.skip("timeline build not present (python -m paper_2412_05693_amd.build --timeline)")
+    code = (
+        "import ctypes\n"
+        "from paper_2412_05693_amd import batchmax as bmx\n"
+        "f = bmx._lib.bm_prefill_timeline\n"
+        "print(f(None, 4), f(ctypes.c_void_p(1), 0), f(ctypes.c_void_p(1), bmx.TIMELINE_MAX_RECORDS + 1))\n")
+    env = dict(os.environ, BATCHMAX_LIB=tl_lib, PYTHONPATH=ROOT)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == [str(bmx.BM_ERR_INVALID_ARG)] * 3

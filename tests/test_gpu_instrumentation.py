@@ -6,6 +6,8 @@
 * The roofline probes (bm_probe.h) run and their sinks hold what the host
   predicts: the XOR of every 32-bit word each workgroup read, and finite
   MFMA sums.
+* The prefill timeline build (a separate library, so a separate process)
+  records one ordered set of timestamps per workgroup of the last launch.
 """
 import numpy as np
 import pytest
@@ -84,3 +86,40 @@ def test_probe_mfma_runs():
     torch.cuda.synchronize()
     s = sink.cpu().numpy()
     assert np.all(np.isfinite(s)) and np.all(s == s[0])
+
+
+def test_prefill_timeline_records():
+    _need_gpu()
+    import os
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    lib = os.path.join(root, "paper_2412_05693_amd", "libbatchmax_timeline.so")
+    if not os.path.exists(lib):
+        pytest.skip("timeline build not present")
+    code = (
+        "import numpy as np, torch\n"
+        "from paper_2412_05693_amd import batchmax as bmx, synth\n"
+        "wl = synth.WORKLOADS['c2'].with_(b=2, s=768, n_decode=1)\n"
+        "q, k, v = synth.batch_inputs(wl, 'cuda'); o = torch.zeros_like(q)\n"
+        "pd = bmx.PDAttention(b=wl.b, s=wl.s, kv_max=wl.kv_max, block=wl.block, max_gen=1,\n"
+        "    n_heads=wl.n_heads, n_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim, dtype=wl.dtype,\n"
+        "    sm_scale=wl.sm_scale, device='cuda')\n"
+        "for t0 in range(0, wl.s, wl.block): pd.prefill_block_cut(t0, wl.block, q, k, v, o)\n"
+        "torch.cuda.synchronize()\n"
+        "nwg = wl.b * wl.n_kv_heads * (wl.block // 32)\n"
+        "r = bmx.bm_prefill_timeline(nwg).astype(np.int64)\n"
+        "mono = np.all(np.diff(r[:, :8], axis=1) >= 0)\n"
+        "units = sorted(set((r[:, 14] >> 32).tolist()))\n"
+        "print(int(mono), int(np.all(r[:, 0] > 0)), len(units), int(r[:, 15].min()), int(r[:, 15].max()))\n")
+    env = dict(os.environ, BATCHMAX_LIB=lib, PYTHONPATH=root)
+    print("[timeline] c2 shape b=2 s=768, last block", flush=True)
+    res = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                         timeout=240)
+    assert res.returncode == 0, res.stderr[-2000:]
+    mono, positive, n_units, tmin, tmax = map(int, res.stdout.split()[-5:])
+    assert mono == 1 and positive == 1
+    assert n_units == 2 * 8
+    # last block: 512 cached keys (8 tiles) + 1..4 block tiles of 64 positions
+    assert tmin == 8 + 1 and tmax == 8 + 4

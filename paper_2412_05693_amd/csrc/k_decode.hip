@@ -77,14 +77,20 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   const E* qbase = static_cast<const E*>(a.q) + ((int64_t)bi * a.n_heads + hk * G) * a.seq_ld * D;
   const float c2 = a.scale_log2;
 
-  // prefetch the scores and positions (used after the softmax) into LDS
-  {
-    const float* score = a.score + (int64_t)u * a.cap;
-    const int32_t* pos = a.pos + (int64_t)u * a.cap;
-    for (int j = tid; j < L; j += 256) {
-      sc[j] = j < len0 ? score[j] : 0.0f;
-      pos_s[j] = j < len0 ? pos[j] : a.cur_pos;
-    }
+  // Scores and positions (used from the softmax on): the first NSP per thread
+  // are loaded into registers here and written to LDS after the logits, so
+  // their latency hides behind the K loads; entries beyond 256 * NSP are
+  // copied after the logits.
+  constexpr int NSP = 4;
+  const float* score_g = a.score + (int64_t)u * a.cap;
+  const int32_t* pos_g = a.pos + (int64_t)u * a.cap;
+  float sp_score[NSP];
+  int32_t sp_pos[NSP];
+#pragma unroll
+  for (int r = 0; r < NSP; ++r) {
+    const int j = min(tid + 256 * r, max(len0 - 1, 0));   // slot 0 exists even when empty
+    sp_score[r] = score_g[j];
+    sp_pos[r] = pos_g[j];
   }
 
   // ---------------- 1. logits ----------------
@@ -93,24 +99,28 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
     bf16x8 qop[D / 32];
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
-      u32x4 qw = {0, 0, 0, 0};
-      if (col < G)
-        qw = *reinterpret_cast<const u32x4*>(qbase + (int64_t)col * a.seq_ld * D + 32 * ks + 8 * g4);
-      qop[ks] = __builtin_bit_cast(bf16x8, qw);
+      // columns G..15 repeat the last head (their results are not stored)
+      const int qc = min(col, G - 1);
+      qop[ks] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(qbase + (int64_t)qc * a.seq_ld * D + 32 * ks + 8 * g4));
     }
     const int ngroups = (L + 15) / 16;
-#pragma unroll 2
-    for (int kg = w; kg < ngroups; kg += 4) {
+    // Keys past the last entry read the step's own key row (valid memory; their
+    // logits are never stored).  With no branch around a load the compiler
+    // can count the loads in flight and wait only for the group it multiplies
+    // while the next group's rows are still arriving.
+    auto k_rows = [&](int kg, u32x4 (&dst)[D / 32]) {
       const int key = kg * 16 + col;
-      const E* src = key < len0 ? kc + (int64_t)key * D : (key == len0 ? knew : nullptr);
-      u32x4 kw[D / 32];
+      const E* src = key < len0 ? kc + (int64_t)key * D : knew;
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks)
-        kw[ks] = src ? *reinterpret_cast<const u32x4*>(src + 32 * ks + 8 * g4) : u32x4{0, 0, 0, 0};
+        dst[ks] = *reinterpret_cast<const u32x4*>(src + 32 * ks + 8 * g4);
+    };
+    auto logits = [&](int kg, const u32x4 (&src)[D / 32]) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks)
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kw[ks]), qop[ks],
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, src[ks]), qop[ks],
                                                       acc, 0, 0, 0);
       if (col < G) {
 #pragma unroll
@@ -119,6 +129,16 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
           if (kk < L) P[col * Lp + kk] = acc[j] * c2;
         }
       }
+    };
+    // two register sets in turn (no copy between them, which would make the
+    // loop wait for the group still in flight)
+    u32x4 ka[D / 32], kb[D / 32];
+    k_rows(w, ka);
+    for (int kg = w; kg < ngroups; kg += 8) {
+      k_rows(kg + 4, kb);
+      logits(kg, ka);
+      k_rows(kg + 8, ka);
+      if (kg + 4 < ngroups) logits(kg + 4, kb);
     }
   } else {
     constexpr int CH = D / 4;               // float4 chunks per row
@@ -144,19 +164,33 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       }
     }
   }
+#pragma unroll
+  for (int r = 0; r < NSP; ++r) {
+    const int j = tid + 256 * r;
+    if (j < L) {
+      sc[j] = j < len0 ? sp_score[r] : 0.0f;
+      pos_s[j] = j < len0 ? sp_pos[r] : a.cur_pos;
+    }
+  }
+  for (int j = tid + 256 * NSP; j < L; j += 256) {
+    sc[j] = j < len0 ? score_g[j] : 0.0f;
+    pos_s[j] = j < len0 ? pos_g[j] : a.cur_pos;
+  }
   __syncthreads();
 
   // first batch of V rows for phase 4, in flight during the softmax
   constexpr int NKL4 = 256 / CPR;
   constexpr int UNR = 8;   // V rows per thread in flight (and as many prefetched)
   const int c4 = tid % CPR, kl4 = tid / CPR;
+  // rows past the last entry read the step's own V row (valid memory, never
+  // used): unconditional loads, so only the batch being consumed is waited for
+  auto v_row = [&](int j) -> u32x4 {
+    const E* src = j < len0 ? vc + (int64_t)j * D : vnew;
+    return load_v<NTV>(src + c4 * EPC);
+  };
   u32x4 vw[UNR];
 #pragma unroll
-  for (int r = 0; r < UNR; ++r) {
-    const int j = kl4 + r * NKL4;
-    const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
-    vw[r] = src ? load_v<NTV>(src + c4 * EPC) : u32x4{0, 0, 0, 0};
-  }
+  for (int r = 0; r < UNR; ++r) vw[r] = v_row(kl4 + r * NKL4);
 
   // ---------------- 2. softmax per query head ----------------
   // (left padding: pad entries, pos < pad, are visible to no query)
@@ -232,11 +266,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       // next batch in flight while this one is consumed
       u32x4 vn[UNR];
 #pragma unroll
-      for (int r = 0; r < UNR; ++r) {
-        const int j = j0 + (UNR + r) * NKL;
-        const E* src = j < len0 ? vc + (int64_t)j * D : (j == len0 ? vnew : nullptr);
-        vn[r] = src ? load_v<NTV>(src + c * EPC) : u32x4{0, 0, 0, 0};
-      }
+      for (int r = 0; r < UNR; ++r) vn[r] = v_row(j0 + (UNR + r) * NKL);
 #pragma unroll
       for (int r = 0; r < UNR; ++r) {
         const int j = j0 + r * NKL;

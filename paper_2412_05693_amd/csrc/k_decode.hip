@@ -8,13 +8,15 @@
 //   1. logits z[g][j] = sm_scale * q_g . k_j for the G query heads, kept in LDS
 //      (bf16: a 16x16x32 MFMA per 16 keys, K rows as the A operand straight
 //      from global memory; f32: VALU dot products);
-//   2. exact softmax per query head (max, sum, normalise) in LDS;
+//   2. exact softmax per query head in LDS (max and sum; each use multiplies
+//      by the reciprocal of the sum);
 //   3. score_j += sum_g P[g][j] (the sum_weights update of Sec. 3.2), ranking
 //      key of the chosen rule (by default ave = score / (pos_now + 1 - pos))
 //      packed with pos into 64 bits, and a workgroup argmin (older entry first
 //      on an exact tie);
-//   4. o_g = sum_j P[g][j] v_j on VALU, V rows read once, 16 bytes per lane
-//      (marked non-temporal when the launch's cached K and V exceed the
+//   4. o_g = sum_j p[g][j] v_j on VALU (exponentials summed, then scaled once
+//      by the reciprocal), V rows read once, 16 bytes per lane (marked
+//      non-temporal when the launch's cached K and V exceed the
 //      device's last-level cache: they are not read again before the next
 //      step has streamed the whole cache through; below that size the next
 //      step finds them in the cache);
@@ -40,6 +42,14 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int off) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// probability = exp2(z - max) * (1 / sum), rounded once and never fused into
+// the sum that uses it (the scores and the ranking see the same value a
+// normalised copy in LDS would hold)
+__device__ __forceinline__ float prob(float e, float inv) {
+#pragma clang fp contract(off)
+  return e * inv;
+}
+
 template <bool NT>
 __device__ __forceinline__ u32x4 load_v(const void* p) {
   if constexpr (NT) {
@@ -57,6 +67,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   extern __shared__ float dsm[];
   __shared__ uint64_t s_wkey[4];
   __shared__ int s_wslot[4];
+  __shared__ float s_inv[4];      // 1 / softmax sum per query head
 
   const int u = blockIdx.x;
   const int bi = u / a.n_kv_heads, hk = u - (u / a.n_kv_heads) * a.n_kv_heads;
@@ -193,31 +204,57 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   for (int r = 0; r < UNR; ++r) vw[r] = v_row(kl4 + r * NKL4);
 
   // ---------------- 2. softmax per query head ----------------
-  // (left padding: pad entries, pos < pad, are visible to no query)
+  // P keeps exp2(z - max) and s_inv[g] = 1 / sum; each use forms the
+  // probability with prob().  Left padding: pad entries (pos < pad) are
+  // visible to no query.
   const int pad = a.pad ? max(0, a.pad[bi]) : 0;
+  constexpr int NSM = 16;   // logits per lane held in registers when L <= 64 * NSM
   for (int g = w; g < G; g += 4) {
     float* pg = P + g * Lp;
-    float m = kNegInf;
-    for (int j = lane; j < L; j += 64) {
-      float x = pg[j];
-      if (pad > 0 && pos_s[j] < pad) {
-        x = kNegInf;
-        pg[j] = x;
-      }
-      m = fmaxf(m, x);
-    }
+    auto visible = [&](int j) { return j < L && !(pad > 0 && pos_s[min(j, L - 1)] < pad); };
+    float m = kNegInf, s = 0.0f;
+    if (L <= 64 * NSM) {
+      // one read of the row with no branch around an LDS read (the pad test
+      // is chosen once), so the reads are issued together
+      float x[NSM];
+      auto load_row = [&](auto padded) {
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-    float s = 0.0f;
-    for (int j = lane; j < L; j += 64) {
-      const float e = __builtin_amdgcn_exp2f(pg[j] - m);
-      pg[j] = e;
-      s += e;
+        for (int i = 0; i < NSM; ++i) {
+          const int j = lane + 64 * i, jc = min(j, L - 1);
+          const float z = pg[jc];
+          bool vis = j < L;
+          if constexpr (decltype(padded)::value) vis = vis && pos_s[jc] >= pad;
+          x[i] = vis ? z : kNegInf;
+        }
+      };
+      if (pad > 0)
+        load_row(std::true_type{});
+      else
+        load_row(std::false_type{});
+#pragma unroll
+      for (int i = 0; i < NSM; ++i) m = fmaxf(m, x[i]);
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+#pragma unroll
+      for (int i = 0; i < NSM; ++i) {
+        const int j = lane + 64 * i;
+        const float e = __builtin_amdgcn_exp2f(x[i] - m);
+        if (j < L) pg[j] = e;
+        s += e;
+      }
+    } else {
+      for (int j = lane; j < L; j += 64) m = fmaxf(m, visible(j) ? pg[j] : kNegInf);
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+      for (int j = lane; j < L; j += 64) {
+        const float e = __builtin_amdgcn_exp2f((visible(j) ? pg[j] : kNegInf) - m);
+        pg[j] = e;
+        s += e;
+      }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-    const float inv = 1.0f / s;
-    for (int j = lane; j < L; j += 64) pg[j] *= inv;
+    if (lane == 0) s_inv[g] = 1.0f / s;
   }
   __syncthreads();
 
@@ -229,7 +266,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
     for (int j = tid; j < L; j += 256) {
       float ps = 0.0f;
 #pragma unroll
-      for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
+      for (int g = 0; g < G; ++g) ps += prob(P[g * Lp + j], s_inv[g]);
       const float s = sc[j] + ps;
       sc[j] = s;
       const uint64_t key = rank_key(a.rule, s, ps, pos_s[j], a.cur_pos);
@@ -253,7 +290,9 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
     }
   }
 
-  // ---------------- 4. outputs o_g = sum_j P[g][j] v_j ----------------
+  // ---------------- 4. outputs o_g = s_inv[g] * sum_j P[g][j] v_j ----------------
+  static_assert(2 * CPR <= 256, "one thread per 16-byte chunk of the new K and V rows");
+  u32x4 nrow;   // this thread's chunk of the step's own K or V row (write back)
   {
     constexpr int NKL = NKL4;
     const int c = c4;
@@ -292,6 +331,11 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int r = 0; r < UNR; ++r) vw[r] = vn[r];
     }
+    // the new rows for the write back, loaded while the outputs are reduced
+    {
+      const int nc = min(tid, 2 * CPR - 1);
+      nrow = *reinterpret_cast<const u32x4*>((nc >= CPR ? vnew : knew) + (nc % CPR) * EPC);
+    }
     // reduce the lanes of a wave that share chunk c, then across waves in LDS
 #pragma unroll
     for (int off = CPR; off < 64; off <<= 1)
@@ -311,8 +355,8 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   // final outputs
   for (int idx = tid; idx < G * D; idx += 256) {
     const int g = idx / D, d = idx - g * D;
-    const float x = red[(0 * G + g) * D + d] + red[(1 * G + g) * D + d] +
-                    red[(2 * G + g) * D + d] + red[(3 * G + g) * D + d];
+    const float x = (red[(0 * G + g) * D + d] + red[(1 * G + g) * D + d] +
+                     red[(2 * G + g) * D + d] + red[(3 * G + g) * D + d]) * s_inv[g];
     E* o = static_cast<E*>(a.o) + (((int64_t)bi * a.n_heads + hk * G + g) * a.seq_ld) * D + d;
     if constexpr (BF16) {
       *o = __builtin_bit_cast(uint16_t, (__bf16)x);
@@ -340,10 +384,9 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   if (dst >= 0 && dst < len0 + (evict ? 0 : 1)) {
     E* kd = static_cast<E*>(a.kc) + ((int64_t)u * a.cap + dst) * D;
     E* vd = static_cast<E*>(a.vc) + ((int64_t)u * a.cap + dst) * D;
-    for (int cidx = tid; cidx < 2 * CPR; cidx += 256) {
-      const int which = cidx / CPR, cc = cidx - which * CPR;
-      const u32x4 x = *reinterpret_cast<const u32x4*>((which ? vnew : knew) + cc * EPC);
-      *reinterpret_cast<u32x4*>((which ? vd : kd) + cc * EPC) = x;
+    if (tid < 2 * CPR) {
+      const int which = tid / CPR, cc = tid - which * CPR;
+      *reinterpret_cast<u32x4*>((which ? vd : kd) + cc * EPC) = nrow;
     }
     if (tid == 0) {
       score[dst] = sc[len0];
@@ -359,7 +402,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       if ((j < len0 && j == dst) || slot < 0 || slot >= len0 + (evict ? 0 : 1)) continue;
       float ps = 0.0f;
 #pragma unroll
-      for (int g = 0; g < G; ++g) ps += P[g * Lp + j];
+      for (int g = 0; g < G; ++g) ps += prob(P[g * Lp + j], s_inv[g]);
       lw[slot] = ps;
     }
   }

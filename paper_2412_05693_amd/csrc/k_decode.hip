@@ -141,15 +141,18 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
         }
       }
     };
-    // two register sets in turn (no copy between them, which would make the
-    // loop wait for the group still in flight)
-    u32x4 ka[D / 32], kb[D / 32];
-    k_rows(w, ka);
-    for (int kg = w; kg < ngroups; kg += 8) {
-      k_rows(kg + 4, kb);
-      logits(kg, ka);
-      k_rows(kg + 8, ka);
-      if (kg + 4 < ngroups) logits(kg + 4, kb);
+    // KD register sets in turn, KD groups in flight (no copy between sets,
+    // which would make the loop wait for a group still in flight)
+    constexpr int KD = 2;
+    u32x4 kr[KD][D / 32];
+#pragma unroll
+    for (int i = 0; i + 1 < KD; ++i) k_rows(w + 4 * i, kr[i]);
+    for (int kg = w; kg < ngroups; kg += 4 * KD) {
+#pragma unroll
+      for (int i = 0; i < KD; ++i) {
+        k_rows(kg + 4 * (i + KD - 1), kr[(i + KD - 1) % KD]);
+        if (i == 0 || kg + 4 * i < ngroups) logits(kg + 4 * i, kr[i]);
+      }
     }
   } else {
     constexpr int CH = D / 4;               // float4 chunks per row

@@ -13,7 +13,9 @@
 //
 // HBM-bound: K and V rows are read once, 16 bytes per lane; a wave load covers
 // 64 / CPR whole rows (CPR 16-byte chunks per row), each row's dot products are
-// finished with shuffles inside its CPR lanes.
+// finished with shuffles inside its CPR lanes; every lane issues four row
+// loads together (whole 1 KB runs per wave instruction, few registers, so
+// many workgroups per compute unit keep the loads in flight).
 #include <type_traits>
 
 #include "bm_internal.h"
@@ -26,21 +28,17 @@ constexpr float kNegInf = -__builtin_huge_valf();
 
 // one 16-byte chunk of a row as floats (8 bf16 or 4 float32 elements)
 template <bool BF16>
-__device__ __forceinline__ void load_chunk(const void* p, float* x) {
+__device__ __forceinline__ void unpack_chunk(const uint4 w, float* x) {
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
   if constexpr (BF16) {
-    const uint4 w = *reinterpret_cast<const uint4*>(p);
-    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       x[2 * i] = __uint_as_float(u[i] << 16);
       x[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
     }
   } else {
-    const float4 w = *reinterpret_cast<const float4*>(p);
-    x[0] = w.x;
-    x[1] = w.y;
-    x[2] = w.z;
-    x[3] = w.w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(u[i]);
   }
 }
 
@@ -79,35 +77,54 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
   __syncthreads();
 
   const int r_in = lane / CPR, ch = lane - r_in * CPR;
-  const int pad = a.pad ? max(0, a.pad[bi]) : 0;
+  // Every row load is unconditional: rows past the chunk's last entry read the
+  // step's own row (valid memory; their results are never stored), so the
+  // compiler can count the loads in flight and wait only for the rows in use.
+  // A lane issues UL row loads together.
+  constexpr int UL = 4;
+  auto k_src = [&](int r) -> const E* { return j0 + r < a.len0 ? kc + (int64_t)(j0 + r) * D : knew; };
+  auto v_src = [&](int r) -> const E* { return j0 + r < a.len0 ? vc + (int64_t)(j0 + r) * D : vnew; };
   // 1. logits: wave w takes row groups w, w + 4, ... of the chunk
-  for (int base = w * RPL; base < nj; base += 4 * RPL) {
-    const int r = base + r_in;
-    const int j = j0 + r;
-    float part[G];
+  for (int base = w * RPL; base < nj; base += 4 * RPL * UL) {
+    uint4 raw[UL];
 #pragma unroll
-    for (int g = 0; g < G; ++g) part[g] = 0.0f;
-    if (r < nj) {
-      const E* row = j < a.len0 ? kc + (int64_t)j * D : knew;
+    for (int i = 0; i < UL; ++i)
+      raw[i] = *reinterpret_cast<const uint4*>(k_src(base + 4 * RPL * i + r_in) + ch * EPC);
+#pragma unroll
+    for (int i = 0; i < UL; ++i) {
+      const int r = base + 4 * RPL * i + r_in;
       float x[EPC];
-      load_chunk<BF16>(row + ch * EPC, x);
+      unpack_chunk<BF16>(raw[i], x);
+      float part[G];
 #pragma unroll
-      for (int g = 0; g < G; ++g)
+      for (int g = 0; g < G; ++g) {
+        part[g] = 0.0f;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) part[g] = fmaf(qs[g][ch * EPC + e], x[e], part[g]);
-    }
+      }
 #pragma unroll
-    for (int off = 1; off < CPR; off <<= 1)
+      for (int off = 1; off < CPR; off <<= 1)
 #pragma unroll
-      for (int g = 0; g < G; ++g) part[g] += __shfl_xor(part[g], off);
-    if (ch == 0 && r < nj) {
-      // left padding: a pad entry (pos < pad) is visible to no query
-      const bool masked = pad > 0 && j < a.len0 && a.pos[(int64_t)u * a.cap + j] < pad;
+        for (int g = 0; g < G; ++g) part[g] += __shfl_xor(part[g], off);
+      if (ch == 0 && r < nj) {
 #pragma unroll
-      for (int g = 0; g < G; ++g) z[g][r] = masked ? kNegInf : part[g];
+        for (int g = 0; g < G; ++g) z[g][r] = part[g];
+      }
     }
   }
   __syncthreads();
+  // left padding: a pad entry (pos < pad) is visible to no query
+  const int pad = a.pad ? max(0, a.pad[bi]) : 0;
+  if (pad > 0) {
+    for (int r = tid; r < nj; r += 256) {
+      const int j = j0 + r;
+      if (j < a.len0 && a.pos[(int64_t)u * a.cap + j] < pad) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) z[g][r] = kNegInf;
+      }
+    }
+    __syncthreads();
+  }
 
   // 2. chunk maximum and exp2 sums, wave g < G handles head g
   if (w < G) {
@@ -138,16 +155,21 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
   for (int g = 0; g < G; ++g)
 #pragma unroll
     for (int e = 0; e < EPC; ++e) acc[g][e] = 0.0f;
-  for (int base = w * RPL; base < nj; base += 4 * RPL) {
-    const int r = base + r_in;
-    if (r < nj) {
-      const int j = j0 + r;
-      const E* row = j < a.len0 ? vc + (int64_t)j * D : vnew;
+  for (int base = w * RPL; base < nj; base += 4 * RPL * UL) {
+    uint4 raw[UL];
+#pragma unroll
+    for (int i = 0; i < UL; ++i)
+      raw[i] = *reinterpret_cast<const uint4*>(v_src(base + 4 * RPL * i + r_in) + ch * EPC);
+#pragma unroll
+    for (int i = 0; i < UL; ++i) {
+      // rows past the chunk's end weigh 0 (their V row is the step's own,
+      // finite): no early exit, so the loads are not moved to their uses
+      const int r = base + 4 * RPL * i + r_in;
       float x[EPC];
-      load_chunk<BF16>(row + ch * EPC, x);
+      unpack_chunk<BF16>(raw[i], x);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        const float p = z[g][r];
+        const float p = r < nj ? z[g][min(r, nj - 1)] : 0.0f;
 #pragma unroll
         for (int e = 0; e < EPC; ++e) acc[g][e] = fmaf(p, x[e], acc[g][e]);
       }

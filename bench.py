@@ -131,12 +131,15 @@ def peak_probe():
 
     nbytes = 4 << 30
     buf = torch.ones(nbytes, dtype=torch.uint8, device=dev)
-    blocks_r = cus * 16
-    sink = torch.empty(blocks_r * 4, dtype=torch.int32, device=dev)
-    for nt in (False, True):
-        t = timed(lambda: bmx.bm_probe_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), blocks_r,
-                                                   nt, stream.cuda_stream), 10)
-        out["stream_read_nt_gb_per_s" if nt else "stream_read_gb_per_s"] = nbytes / t / 1e9
+    sink = torch.empty(cus * 16, dtype=torch.int32, device=dev)
+    # one workgroup per compute unit sweeping the buffer together, and 16 per
+    # compute unit (more than can be resident at once)
+    for per_cu in (1, 16):
+        for nt in (False, True):
+            t = timed(lambda: bmx.bm_probe_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(),
+                                                       cus * per_cu, nt, stream.cuda_stream), 10)
+            key = f"stream_read{'_nt' if nt else ''}_{per_cu}wg_per_cu_gb_per_s"
+            out[key] = nbytes / t / 1e9
     del buf
     for waves_per_cu in (8, 16):
         blocks_m, iters = cus * waves_per_cu // 4, 20000

@@ -24,7 +24,7 @@ extern "C" {
 
 /* Read `bytes` bytes at `src` (device memory, 16-byte aligned, bytes a
  * multiple of 16) once, 16 bytes per lane, `blocks` workgroups of 256 threads
- * striding over the buffer; each workgroup writes one 32-bit word of the XOR of
+ * striding over the buffer, eight loads per lane in flight; each workgroup writes one 32-bit word of the XOR of
  * what it read to sink[blockIdx] (`sink`: `blocks` words of device memory), so
  * the loads cannot be dropped.  nontemporal = 1 marks the loads as streaming
  * (not kept in the caches).  BM_ERR_INVALID_ARG for a null pointer, a

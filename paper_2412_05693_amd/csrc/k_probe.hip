@@ -19,7 +19,9 @@ __device__ __forceinline__ u32x4 load16(const u32x4* p) {
   }
 }
 
-// grid-stride read, four 16-byte loads in flight per lane per round
+// grid-stride read, kReadRound 16-byte loads in flight per lane per round
+// (eight: with fewer the read rate depends on the grid size)
+constexpr int kReadRound = 8;
 template <bool NT>
 __global__ void __launch_bounds__(256) probe_read_kernel(const u32x4* src, size_t n16,
                                                          uint32_t* sink) {
@@ -27,13 +29,12 @@ __global__ void __launch_bounds__(256) probe_read_kernel(const u32x4* src, size_
   const size_t stride = (size_t)gridDim.x * 256;
   size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   uint32_t acc = 0;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const u32x4 a = load16<NT>(src + i);
-    const u32x4 b = load16<NT>(src + i + stride);
-    const u32x4 c = load16<NT>(src + i + 2 * stride);
-    const u32x4 d = load16<NT>(src + i + 3 * stride);
-    acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^
-           (d.x ^ d.y ^ d.z ^ d.w);
+  for (; i + (kReadRound - 1) * stride < n16; i += kReadRound * stride) {
+    u32x4 v[kReadRound];
+#pragma unroll
+    for (int k = 0; k < kReadRound; ++k) v[k] = load16<NT>(src + i + k * stride);
+#pragma unroll
+    for (int k = 0; k < kReadRound; ++k) acc ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
   }
   for (; i < n16; i += stride) {
     const u32x4 a = load16<NT>(src + i);

@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
   const int len0 = a.len0;
   const int L = len0 + 1;
   const int Lp = (L + 3) & ~3;
-  float* P = dsm;                 // [G][Lp] logits, then probabilities
+  float* P = dsm;                 // [G][Lp] logits, then exp2(logit - max)
   float* sc = P + G * Lp;         // [Lp] scores (prefetched, then updated)
   float* red = sc + Lp;           // [4][G][D] partial outputs per wave
   int32_t* pos_s = reinterpret_cast<int32_t*>(red + 4 * G * D);   // [Lp] positions

@@ -36,9 +36,84 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int off) {
-  const uint32_t lo = __shfl_xor((uint32_t)x, off);
-  const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), off);
+// Wave-wide reductions without LDS round trips: quad permutes for lanes 1 and
+// 2 apart, the mirrored halves of each 8- and 16-lane row (DPP), then gfx950's
+// swaps of the 16- and 32-lane halves.  Each step combines two disjoint lane
+// groups that already agree on their own result, so every lane ends with the
+// wave's.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t x) {
+  return __builtin_amdgcn_update_dpp(x, x, CTRL, 0xF, 0xF, false);
+}
+
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, Op op) {
+  x = op(x, dpp<0xB1>(x));    // quad_perm [1,0,3,2]
+  x = op(x, dpp<0x4E>(x));    // quad_perm [2,3,0,1]
+  x = op(x, dpp<0x141>(x));   // row_half_mirror
+  x = op(x, dpp<0x140>(x));   // row_mirror
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = op(a[0], a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return op(b[0], b[1]);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  return __uint_as_float(wave_reduce(__float_as_uint(v), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  return __uint_as_float(wave_reduce(__float_as_uint(v), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
+}
+
+// v plus the value of the lane OFF apart (lane ^ OFF) for OFF = 8, 16, 32: a
+// row rotation by 8 inside each 16-lane row, gfx950's half swaps for 16 and 32
+template <int OFF>
+__device__ __forceinline__ float add_xor(float v) {
+  const uint32_t x = __float_as_uint(v);
+  if constexpr (OFF == 8) {
+    return v + __uint_as_float(dpp<0x128>(x));   // row_ror:8
+  } else if constexpr (OFF == 16) {
+    const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  } else {
+    static_assert(OFF == 32, "lane offsets 8, 16 or 32");
+    const auto a = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  }
+}
+
+// smallest 64-bit key of the wave (the same steps on both halves of the key)
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
+  uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
+  auto take = [&](uint32_t plo, uint32_t phi) {
+    if ((((uint64_t)phi << 32) | plo) < (((uint64_t)hi << 32) | lo)) {
+      lo = plo;
+      hi = phi;
+    }
+  };
+  take(dpp<0xB1>(lo), dpp<0xB1>(hi));
+  take(dpp<0x4E>(lo), dpp<0x4E>(hi));
+  take(dpp<0x141>(lo), dpp<0x141>(hi));
+  take(dpp<0x140>(lo), dpp<0x140>(hi));
+  {
+    const auto a = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto b = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    lo = a[0];
+    hi = b[0];
+    take(a[1], b[1]);
+  }
+  {
+    const auto a = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+    lo = a[0];
+    hi = b[0];
+    take(a[1], b[1]);
+  }
   return ((uint64_t)hi << 32) | lo;
 }
 
@@ -236,8 +311,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
         load_row(std::false_type{});
 #pragma unroll
       for (int i = 0; i < NSM; ++i) m = fmaxf(m, x[i]);
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+      m = wave_max(m);
 #pragma unroll
       for (int i = 0; i < NSM; ++i) {
         const int j = lane + 64 * i;
@@ -247,16 +321,14 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       }
     } else {
       for (int j = lane; j < L; j += 64) m = fmaxf(m, visible(j) ? pg[j] : kNegInf);
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+      m = wave_max(m);
       for (int j = lane; j < L; j += 64) {
         const float e = __builtin_amdgcn_exp2f((visible(j) ? pg[j] : kNegInf) - m);
         pg[j] = e;
         s += e;
       }
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    s = wave_sum(s);
     if (lane == 0) s_inv[g] = 1.0f / s;
   }
   __syncthreads();
@@ -278,15 +350,12 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
         bslot = j;
       }
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const uint64_t ob = shfl_xor_u64(best, off);
-      const int os = __shfl_xor(bslot, off);
-      if (ob < best) {
-        best = ob;
-        bslot = os;
-      }
-    }
+    // the wave's smallest key (unique: it carries the entry's position) and
+    // the slot of the lane that holds it
+    const uint64_t wmin = wave_min_u64(best);
+    const uint64_t holders = __ballot(best == wmin);
+    bslot = __builtin_amdgcn_readlane(bslot, (int)__builtin_ctzll(holders));
+    best = wmin;
     if (lane == 0) {
       s_wkey[w] = best;
       s_wslot[w] = bslot;
@@ -339,13 +408,18 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       const int nc = min(tid, 2 * CPR - 1);
       nrow = *reinterpret_cast<const u32x4*>((nc >= CPR ? vnew : knew) + (nc % CPR) * EPC);
     }
-    // reduce the lanes of a wave that share chunk c, then across waves in LDS
+    // reduce the lanes of a wave that share chunk c (lanes c, c + CPR, ...),
+    // then across waves in LDS
+    static_assert(CPR == 8 || CPR == 16 || CPR == 32, "16-byte chunks per row");
 #pragma unroll
-    for (int off = CPR; off < 64; off <<= 1)
+    for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+      for (int e = 0; e < EPC; ++e) {
+        float x = acc[g][e];
+        if constexpr (CPR <= 8) x = add_xor<8>(x);
+        if constexpr (CPR <= 16) x = add_xor<16>(x);
+        acc[g][e] = add_xor<32>(x);
+      }
     if (lane < CPR) {
 #pragma unroll
       for (int g = 0; g < G; ++g)

@@ -26,96 +26,21 @@
 #include <type_traits>
 
 #include "bm_internal.h"
+#include "bm_lanes.h"
 
 namespace bm {
 namespace {
+
+using lanes::add_xor;
+using lanes::wave_max;
+using lanes::wave_min_u64;
+using lanes::wave_sum;
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr float kNegInf = -__builtin_huge_valf();
-
-// Wave-wide reductions without LDS round trips: quad permutes for lanes 1 and
-// 2 apart, the mirrored halves of each 8- and 16-lane row (DPP), then gfx950's
-// swaps of the 16- and 32-lane halves.  Each step combines two disjoint lane
-// groups that already agree on their own result, so every lane ends with the
-// wave's.
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp(uint32_t x) {
-  return __builtin_amdgcn_update_dpp(x, x, CTRL, 0xF, 0xF, false);
-}
-
-template <typename Op>
-__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, Op op) {
-  x = op(x, dpp<0xB1>(x));    // quad_perm [1,0,3,2]
-  x = op(x, dpp<0x4E>(x));    // quad_perm [2,3,0,1]
-  x = op(x, dpp<0x141>(x));   // row_half_mirror
-  x = op(x, dpp<0x140>(x));   // row_mirror
-  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-  x = op(a[0], a[1]);
-  const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-  return op(b[0], b[1]);
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-  return __uint_as_float(wave_reduce(__float_as_uint(v), [](uint32_t a, uint32_t b) {
-    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
-  }));
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-  return __uint_as_float(wave_reduce(__float_as_uint(v), [](uint32_t a, uint32_t b) {
-    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
-  }));
-}
-
-// v plus the value of the lane OFF apart (lane ^ OFF) for OFF = 8, 16, 32: a
-// row rotation by 8 inside each 16-lane row, gfx950's half swaps for 16 and 32
-template <int OFF>
-__device__ __forceinline__ float add_xor(float v) {
-  const uint32_t x = __float_as_uint(v);
-  if constexpr (OFF == 8) {
-    return v + __uint_as_float(dpp<0x128>(x));   // row_ror:8
-  } else if constexpr (OFF == 16) {
-    const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-    return __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  } else {
-    static_assert(OFF == 32, "lane offsets 8, 16 or 32");
-    const auto a = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-    return __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  }
-}
-
-// smallest 64-bit key of the wave (the same steps on both halves of the key)
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
-  uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
-  auto take = [&](uint32_t plo, uint32_t phi) {
-    if ((((uint64_t)phi << 32) | plo) < (((uint64_t)hi << 32) | lo)) {
-      lo = plo;
-      hi = phi;
-    }
-  };
-  take(dpp<0xB1>(lo), dpp<0xB1>(hi));
-  take(dpp<0x4E>(lo), dpp<0x4E>(hi));
-  take(dpp<0x141>(lo), dpp<0x141>(hi));
-  take(dpp<0x140>(lo), dpp<0x140>(hi));
-  {
-    const auto a = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
-    const auto b = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
-    lo = a[0];
-    hi = b[0];
-    take(a[1], b[1]);
-  }
-  {
-    const auto a = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
-    const auto b = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
-    lo = a[0];
-    hi = b[0];
-    take(a[1], b[1]);
-  }
-  return ((uint64_t)hi << 32) | lo;
-}
 
 // probability = exp2(z - max) * (1 / sum), rounded once and never fused into
 // the sum that uses it (the scores and the ranking see the same value a
@@ -247,8 +172,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float part = qr[g].x * kv.x + qr[g].y * kv.y + qr[g].z * kv.z + qr[g].w * kv.w;
-#pragma unroll
-        for (int off = CH / 2; off > 0; off >>= 1) part += __shfl_xor(part, off);
+        part = lanes::group_sum<CH>(part);
         if (c == 0 && j < L) P[g * Lp + j] = part * c2;
       }
     }

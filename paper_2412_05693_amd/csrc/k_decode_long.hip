@@ -19,6 +19,7 @@
 #include <type_traits>
 
 #include "bm_internal.h"
+#include "bm_lanes.h"
 
 namespace bm {
 namespace {
@@ -103,9 +104,7 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
         for (int e = 0; e < EPC; ++e) part[g] = fmaf(qs[g][ch * EPC + e], x[e], part[g]);
       }
 #pragma unroll
-      for (int off = 1; off < CPR; off <<= 1)
-#pragma unroll
-        for (int g = 0; g < G; ++g) part[g] += __shfl_xor(part[g], off);
+      for (int g = 0; g < G; ++g) part[g] = lanes::group_sum<CPR>(part[g]);
       if (ch == 0 && r < nj) {
 #pragma unroll
         for (int g = 0; g < G; ++g) z[g][r] = part[g];
@@ -130,8 +129,7 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
   if (w < G) {
     float m = kNegInf;
     for (int r = lane; r < nj; r += 64) m = fmaxf(m, z[w][r]);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    m = lanes::wave_max(m);
     float l = 0.0f;
     for (int r = lane; r < nj; r += 64) {
       // a chunk of pad entries only: no weight (m = -inf)
@@ -139,8 +137,7 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
       z[w][r] = p;
       l += p;
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) l += __shfl_xor(l, off);
+    l = lanes::wave_sum(l);
     if (lane == 0) {
       s_m[w] = m;
       s_l[w] = l;
@@ -176,12 +173,16 @@ __global__ void __launch_bounds__(256) decode_split_kernel(LongDecodeArgs a) {
     }
   }
   // sum over the RPL rows of a wave load (lanes ch, ch + CPR, ...)
+  static_assert(CPR == 8 || CPR == 16 || CPR == 32, "16-byte chunks per row");
 #pragma unroll
-  for (int off = CPR; off < 64; off <<= 1)
+  for (int g = 0; g < G; ++g)
 #pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+    for (int e = 0; e < EPC; ++e) {
+      float x = acc[g][e];
+      if constexpr (CPR <= 8) x = lanes::add_xor<8>(x);
+      if constexpr (CPR <= 16) x = lanes::add_xor<16>(x);
+      acc[g][e] = lanes::add_xor<32>(x);
+    }
   if (r_in == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g)

@@ -93,6 +93,30 @@ def test_degenerate_bounds(case):
     assert st.cuts > 0
 
 
+@pytest.mark.parametrize("case", [
+    # the largest block the library takes (1024 tokens: 32 position tiles per
+    # unit at G = 4), a ragged last block, both cut paths
+    dict(name="maxblock", b=1, n_heads=4, n_kv_heads=1, s=2300, kv_max=1000, block=1024,
+         n_decode=3, fused_cut=False),
+    dict(name="maxblock", b=1, n_heads=4, n_kv_heads=1, s=2300, kv_max=1000, block=1024,
+         n_decode=3, fused_cut=True),
+    # the same at G = 1 in fp32 with d = 64 (128 positions per workgroup)
+    dict(name="maxblock", dtype="f32", b=1, n_heads=2, n_kv_heads=2, head_dim=64, s=1500,
+         kv_max=600, block=1024, n_decode=2, fused_cut=True),
+    # decode steps over exactly 4097 entries, the most the fused decode kernel
+    # attends to in one workgroup (4096 cached, full, plus the step's own pair)
+    dict(name="decode4097", b=1, n_heads=4, n_kv_heads=1, s=4096, kv_max=4096, block=512,
+         n_decode=3, fused_cut=True),
+], ids=lambda c: f"{c['name']}-{c.get('dtype', 'bf16')}-B{c['block']}-kv{c['kv_max']}-"
+                 f"{'fused' if c['fused_cut'] else 'separate'}")
+def test_maximum_sizes(case):
+    case = dict(case)
+    fused = case.pop("fused_cut")
+    wl = C2.with_(hh_mode="scatter", n_sinks=4, **case)
+    st = _run(wl, synth.checked_units(wl, wl.units), fused_cut=fused)
+    assert st.cuts > 0
+
+
 def test_no_eviction_dense_fixed_point():
     # bound >= s + D: nothing is ever evicted, every output is dense causal attention
     wl = C2.with_(b=2, s=600, kv_max=700, block=256, n_decode=10)

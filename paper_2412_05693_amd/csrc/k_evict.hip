@@ -197,6 +197,8 @@ __global__ void __launch_bounds__(256) compact_kernel(EvictArgs a, int nchunks) 
 // three).  The folded scores, the positions and TOVA's weights stay in LDS, the
 // keys in registers; the hole and source lists are built in LDS; the moves copy
 // K and V rows with 16-byte loads and stores.  Needs n <= kMaxCap.
+// KP: keys per thread held in registers (n <= 256 KP)
+template <int KP>
 __global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs a,
                                                         int pt_positions) {
   __shared__ uint32_t hist[256];
@@ -220,28 +222,81 @@ __global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs
   float* last = a.rule == BM_RANK_TOVA ? a.lastw + (int64_t)u * a.cap : nullptr;
   const float* part = pa.partial + (int64_t)u * pa.npt_stride * pa.cap;
 
-  // 1. fold the partial sums (workgroup order, as score_reduce_kernel) and key
-  uint64_t key[kMaxPer];
+  // 1. fold the partial sums (workgroup order, as score_reduce_kernel) and key.
+  //    Four entries at a time, every load of a round is issued before any is
+  //    used: addresses are clamped into range (an unused term reads a row the
+  //    entry needs anyway) and unused terms are selected to zero, so no load
+  //    sits behind a branch and the sums keep their order (adding +0 changes
+  //    nothing: the sums are >= 0).
+  constexpr int FK = 4;    // entries per round
+  constexpr int PTC = 8;   // partial rows per round
+  static_assert(KP % FK == 0, "whole rounds");
+  uint64_t key[KP];
+  const int nlast = n - 1;
+  const int npt_used = pa.accumulate ? pa.npt_used : 0;
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i) {
-    const int j = tid + 256 * i;
-    key[i] = ~0ull;
-    if (i < per && j < n) {
-      const int pt0 = j < pa.len0 ? 0 : (j - pa.len0) / pt_positions;
-      float acc = j < pa.len0 ? score[j] : 0.0f;
-      if (pa.accumulate) {
-#pragma unroll 8
-        for (int pt = pt0; pt < pa.npt_used; ++pt) acc += part[(int64_t)pt * pa.cap + j];
+  for (int i0 = 0; i0 < KP; i0 += FK) {
+    if (i0 >= per) break;   // uniform across the workgroup
+    float acc[FK], l[FK], sc0[FK];
+    int p[FK], pt0[FK];
+    float x[FK][PTC];
+    // partial row of term c0 + c, clamped into the rows the entry has (or row
+    // 0 of the workspace when nothing accumulates)
+    auto load_terms = [&](int c0) {
+#pragma unroll
+      for (int f = 0; f < FK; ++f) {
+        const int jc = min(tid + 256 * (i0 + f), nlast);
+#pragma unroll
+        for (int c = 0; c < PTC; ++c) {
+          const int pt = min(max(c0 + c, pt0[f]), max(npt_used - 1, 0));
+          x[f][c] = part[(int64_t)pt * pa.cap + jc];
+        }
       }
-      const int p = pos[j];
-      const float l = last ? last[j] : 0.0f;
-      score[j] = acc;
-      sc[j] = acc;
-      ps[j] = p;
-      lw[j] = l;
-      key[i] = rank_key(a.rule, acc, l, p, a.curr_id);
+    };
+    auto add_terms = [&](int c0) {
+#pragma unroll
+      for (int f = 0; f < FK; ++f)
+#pragma unroll
+        for (int c = 0; c < PTC; ++c) {
+          const int pt = c0 + c;
+          acc[f] += pt >= pt0[f] && pt < npt_used ? x[f][c] : 0.0f;
+        }
+    };
+#pragma unroll
+    for (int f = 0; f < FK; ++f) {
+      const int jc = min(tid + 256 * (i0 + f), nlast);
+      pt0[f] = jc < pa.len0 ? 0 : (jc - pa.len0) / pt_positions;
+      sc0[f] = score[jc];
+      p[f] = pos[jc];
+      l[f] = last ? last[jc] : 0.0f;
+    }
+    load_terms(0);   // issued with the loads above, before any of them is used
+#pragma unroll
+    for (int f = 0; f < FK; ++f) {
+      const int jc = min(tid + 256 * (i0 + f), nlast);
+      acc[f] = jc < pa.len0 ? sc0[f] : 0.0f;
+    }
+    add_terms(0);
+    for (int c0 = PTC; c0 < npt_used; c0 += PTC) {
+      load_terms(c0);
+      add_terms(c0);
+    }
+#pragma unroll
+    for (int f = 0; f < FK; ++f) {
+      const int i = i0 + f, j = tid + 256 * i;
+      key[i] = ~0ull;
+      if (i < per && j < n) {
+        score[j] = acc[f];
+        sc[j] = acc[f];
+        ps[j] = p[f];
+        lw[j] = l[f];
+        key[i] = rank_key(a.rule, acc[f], l[f], p[f], a.curr_id);
+      }
     }
   }
+#pragma unroll
+  for (int i = 0; i < KP; ++i)
+    if (i >= per) key[i] = ~0ull;
   if (n <= a.kv_max) {
     if (tid == 0) a.len[u] = n;
     return;
@@ -249,10 +304,10 @@ __global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs
 
   // 2. the cut: the (n - kv_max)-th smallest key, then holes and sources
   auto key_of = [&](int i) __device__ -> uint64_t { return key[i]; };
-  const uint64_t thr = radix_kth(key_of, kMaxPer, per, n, n - a.kv_max, hist, &s_prefix, &s_need);
+  const uint64_t thr = radix_kth(key_of, KP, per, n, n - a.kv_max, hist, &s_prefix, &s_need);
   int hbase = 0, sbase = 0;
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i) {
+  for (int i = 0; i < KP; ++i) {
     if (i >= per) break;  // uniform across the workgroup
     const int j = tid + 256 * i;
     const bool live = j < n;
@@ -299,8 +354,12 @@ hipError_t launch_fold_cut(const PrefillArgs& pa, const EvictArgs& a, int pt_pos
                            hipStream_t stream) {
   if (a.n > kMaxCap) return hipErrorInvalidValue;
   const size_t lds = 5 * sizeof(int32_t) * (size_t)((a.n + 3) & ~3);
-  hipLaunchKernelGGL(fold_cut_kernel, dim3((unsigned)a.units), dim3(256), lds, stream, pa, a,
-                     pt_positions);
+  if (a.n <= 256 * 4)
+    hipLaunchKernelGGL(fold_cut_kernel<4>, dim3((unsigned)a.units), dim3(256), lds, stream, pa, a,
+                       pt_positions);
+  else
+    hipLaunchKernelGGL(fold_cut_kernel<kMaxPer>, dim3((unsigned)a.units), dim3(256), lds, stream, pa,
+                       a, pt_positions);
   return hipGetLastError();
 }
 

@@ -44,31 +44,40 @@ __device__ __forceinline__ int block_excl_count(bool flag, int* s_wave, int* tot
 }
 
 // The need-th smallest (1-based) of the keys key_of(i) of the entries
-// tid + 256 i < n: an 8-pass radix select over 8-bit digits (histograms in LDS,
-// a 64-lane scan of the 256 bins).  Keys are unique (they hold the position),
-// so exactly `need` keys are <= the result.
+// tid + 256 i < n: a radix select over 8-bit digits (histograms in LDS, a
+// 64-lane scan of the 256 bins).  Keys are unique (they hold the position), so
+// exactly `need` keys are <= the result.  The low 32 bits of every key are the
+// entry's position, which is at most curr_id: the digits of that word at and
+// above bit pos_bits are zero in every key, so their passes are skipped (they
+// would keep the prefix and `need` as they are).  The two 256-bin histograms
+// alternate between the passes, so clearing the next one needs no barrier of
+// its own: two barriers per pass.
 template <typename KeyOf>
 __device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per, int n, int need,
-                                              uint32_t* hist, uint64_t* s_prefix, int* s_need) {
+                                              int pos_bits, uint32_t* hist, uint64_t* s_prefix,
+                                              int* s_need) {
   const int tid = threadIdx.x;
   uint64_t prefix = 0;
+  hist[tid] = 0;
+  __syncthreads();
+  int q = 0;   // passes run so far
   for (int pass = 0; pass < 8; ++pass) {
     const int shift = 56 - 8 * pass;
+    if (shift < 32 && shift >= pos_bits) continue;   // uniform across the workgroup
     const uint64_t himask = pass == 0 ? 0ull : (~0ull << (shift + 8));
-    hist[tid] = 0;
-    __syncthreads();
+    uint32_t* h = hist + 256 * (q & 1);
 #pragma unroll
     for (int i = 0; i < n_iter; ++i) {
       const int j = tid + 256 * i;
       if (i < per && j < n) {
         const uint64_t kk = key_of(i);
-        if ((kk & himask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
+        if ((kk & himask) == prefix) atomicAdd(&h[(kk >> shift) & 255u], 1u);
       }
     }
+    hist[256 * ((q + 1) & 1) + tid] = 0;   // the next pass's histogram
     __syncthreads();
     if (tid < 64) {
-      const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
-                     h3 = hist[4 * tid + 3];
+      const uint32_t h0 = h[4 * tid], h1 = h[4 * tid + 1], h2 = h[4 * tid + 2], h3 = h[4 * tid + 3];
       const uint32_t mine = h0 + h1 + h2 + h3;
       uint32_t incl = mine;
 #pragma unroll
@@ -90,16 +99,77 @@ __device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per,
     __syncthreads();
     prefix = *s_prefix;
     need = *s_need;
+    ++q;
   }
   return prefix;
 }
 
+// bits that hold every position of a cut ranked at curr_id (positions <= curr_id)
+__device__ __forceinline__ int position_bits(int curr_id) {
+  return curr_id > 0 ? 32 - __clz(curr_id) : 0;
+}
+
+// The hole list (evicted slots below kv_max) and the source list (kept slots at
+// or above kv_max), both in slot order, slot j = tid + 256 i for i < per <=
+// kMaxPer.  Each wave counts its holes and sources of every i with ballots;
+// the counts (holes in the low 16 bits, sources in the high) go through LDS
+// once and one wave scans them, so the lists take two barriers whatever `per`
+// is.  evicted(i): the entry in slot tid + 256 i is evicted (false past n);
+// emit(is_hole, index, slot) stores one list entry.
+template <typename Evicted, typename Emit>
+__device__ __forceinline__ void build_lists(Evicted evicted, int n_iter, int per, int n, int kv_max,
+                                            uint32_t* s_cnt, int* s_tot, Emit emit) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+  for (int i = 0; i < n_iter; ++i) {
+    if (i < per) {
+      const int j = tid + 256 * i;
+      const bool live = j < n, ev = live && evicted(i);
+      const uint64_t bh = __ballot(live && j < kv_max && ev);
+      const uint64_t bs = __ballot(live && j >= kv_max && !ev);
+      if (lane == 0) s_cnt[4 * i + w] = (uint32_t)__popcll(bh) | ((uint32_t)__popcll(bs) << 16);
+    }
+  }
+  __syncthreads();
+  if (tid < 64) {
+    // exclusive prefix over (i, wave) in slot order; both fields stay below 2^16
+    const uint32_t mine = tid < 4 * per ? s_cnt[tid] : 0u;
+    uint32_t incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t o = __shfl_up(incl, off);
+      if (tid >= off) incl += o;
+    }
+    if (tid < 4 * per) s_cnt[tid] = incl - mine;
+    if (tid == 63) {
+      s_tot[0] = (int)(incl & 0xFFFFu);
+      s_tot[1] = (int)(incl >> 16);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < n_iter; ++i) {
+    if (i < per) {
+      const int j = tid + 256 * i;
+      const bool live = j < n, ev = live && evicted(i);
+      const bool is_hole = live && j < kv_max && ev, is_src = live && j >= kv_max && !ev;
+      const uint64_t bh = __ballot(is_hole), bs = __ballot(is_src);
+      const uint32_t base = s_cnt[4 * i + w];
+      if (is_hole) emit(true, (int)(base & 0xFFFFu) + __popcll(bh & below), j);
+      if (is_src) emit(false, (int)(base >> 16) + __popcll(bs & below), j);
+    }
+  }
+}
+
 template <bool STREAM>
 __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[512];
   __shared__ uint64_t s_prefix;
   __shared__ int s_need;
   __shared__ int s_wave[4];
+  __shared__ uint32_t s_cnt[4 * kMaxPer];
+  __shared__ int s_tot[2];
   const int u = blockIdx.x;
   const int tid = threadIdx.x;
   const float* score = a.score + (int64_t)u * a.cap;
@@ -127,28 +197,34 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
     }
   };
   const int n_iter = STREAM ? per : kMaxPer;
-  const uint64_t thr = radix_kth(key_of, n_iter, per, a.n, a.n - a.kv_max, hist, &s_prefix,
-                                 &s_need);   // exactly n - kv_max keys are <= thr
+  const uint64_t thr = radix_kth(key_of, n_iter, per, a.n, a.n - a.kv_max, position_bits(a.curr_id),
+                                 hist, &s_prefix, &s_need);   // exactly n - kv_max keys are <= thr
 
   // holes (evicted, slot < kv_max) and sources (kept, slot >= kv_max), slot order
   int32_t* holes = a.holes + (int64_t)u * a.cap;
   int32_t* srcs = a.srcs + (int64_t)u * a.cap;
   int hbase = 0, sbase = 0;
-#pragma unroll
-  for (int i = 0; i < n_iter; ++i) {
-    if (i >= per) break;  // uniform across the workgroup
-    const int j = tid + 256 * i;
-    const bool live = j < a.n;
-    const bool ev = live && key_of(i) <= thr;
-    const bool is_hole = live && j < a.kv_max && ev;
-    const bool is_src = live && j >= a.kv_max && !ev;
-    int ht, stot;
-    const int hr = block_excl_count(is_hole, s_wave, &ht);
-    const int sr = block_excl_count(is_src, s_wave, &stot);
-    if (is_hole) holes[hbase + hr] = j;
-    if (is_src) srcs[sbase + sr] = j;
-    hbase += ht;
-    sbase += stot;
+  if constexpr (STREAM) {
+    // more than kMaxPer entries per thread: one workgroup count per 256 slots
+    for (int i = 0; i < per; ++i) {
+      const int j = tid + 256 * i;
+      const bool live = j < a.n;
+      const bool ev = live && key_of(i) <= thr;
+      const bool is_hole = live && j < a.kv_max && ev;
+      const bool is_src = live && j >= a.kv_max && !ev;
+      int ht, stot;
+      const int hr = block_excl_count(is_hole, s_wave, &ht);
+      const int sr = block_excl_count(is_src, s_wave, &stot);
+      if (is_hole) holes[hbase + hr] = j;
+      if (is_src) srcs[sbase + sr] = j;
+      hbase += ht;
+      sbase += stot;
+    }
+  } else {
+    build_lists([&](int i) { return key_of(i) <= thr; }, n_iter, per, a.n, a.kv_max, s_cnt, s_tot,
+                [&](bool hole, int idx, int j) { (hole ? holes : srcs)[idx] = j; });
+    hbase = s_tot[0];
+    sbase = s_tot[1];
   }
   if (tid == 0) {
     a.mcount[u] = min(hbase, sbase);
@@ -201,10 +277,11 @@ __global__ void __launch_bounds__(256) compact_kernel(EvictArgs a, int nchunks) 
 template <int KP>
 __global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs a,
                                                         int pt_positions) {
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[512];
   __shared__ uint64_t s_prefix;
   __shared__ int s_need;
-  __shared__ int s_wave[4];
+  __shared__ uint32_t s_cnt[4 * kMaxPer];
+  __shared__ int s_tot[2];
   // per-slot LDS arrays, n4 = n rounded up to 4 entries each (dynamic size)
   extern __shared__ __attribute__((aligned(16))) char k7_lds[];
   const int n = a.n;
@@ -304,24 +381,11 @@ __global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs
 
   // 2. the cut: the (n - kv_max)-th smallest key, then holes and sources
   auto key_of = [&](int i) __device__ -> uint64_t { return key[i]; };
-  const uint64_t thr = radix_kth(key_of, KP, per, n, n - a.kv_max, hist, &s_prefix, &s_need);
-  int hbase = 0, sbase = 0;
-#pragma unroll
-  for (int i = 0; i < KP; ++i) {
-    if (i >= per) break;  // uniform across the workgroup
-    const int j = tid + 256 * i;
-    const bool live = j < n;
-    const bool ev = live && key[i] <= thr;
-    const bool is_hole = live && j < a.kv_max && ev;
-    const bool is_src = live && j >= a.kv_max && !ev;
-    int ht, stot;
-    const int hr = block_excl_count(is_hole, s_wave, &ht);
-    const int sr = block_excl_count(is_src, s_wave, &stot);
-    if (is_hole) holes[hbase + hr] = j;
-    if (is_src) srcs[sbase + sr] = j;
-    hbase += ht;
-    sbase += stot;
-  }
+  const uint64_t thr = radix_kth(key_of, KP, per, n, n - a.kv_max, position_bits(a.curr_id), hist,
+                                 &s_prefix, &s_need);
+  build_lists([&](int i) { return key[i] <= thr; }, KP, per, n, a.kv_max, s_cnt, s_tot,
+              [&](bool hole, int idx, int j) { (hole ? holes : srcs)[idx] = j; });
+  const int hbase = s_tot[0], sbase = s_tot[1];
   __syncthreads();
 
   // 3. the moves: the i-th source into the i-th hole (disjoint slot ranges)

@@ -305,8 +305,8 @@ __global__ void __launch_bounds__(256) fold_cut_kernel(PrefillArgs pa, EvictArgs
   //    entry needs anyway) and unused terms are selected to zero, so no load
   //    sits behind a branch and the sums keep their order (adding +0 changes
   //    nothing: the sums are >= 0).
-  constexpr int FK = 4;    // entries per round
-  constexpr int PTC = 8;   // partial rows per round
+  constexpr int FK = KP < 4 ? KP : 4;   // entries per round
+  constexpr int PTC = 8;                // partial rows per round
   static_assert(KP % FK == 0, "whole rounds");
   uint64_t key[KP];
   const int nlast = n - 1;
@@ -418,7 +418,10 @@ hipError_t launch_fold_cut(const PrefillArgs& pa, const EvictArgs& a, int pt_pos
                            hipStream_t stream) {
   if (a.n > kMaxCap) return hipErrorInvalidValue;
   const size_t lds = 5 * sizeof(int32_t) * (size_t)((a.n + 3) & ~3);
-  if (a.n <= 256 * 4)
+  if (a.n <= 256 * 3)
+    hipLaunchKernelGGL(fold_cut_kernel<3>, dim3((unsigned)a.units), dim3(256), lds, stream, pa, a,
+                       pt_positions);
+  else if (a.n <= 256 * 4)
     hipLaunchKernelGGL(fold_cut_kernel<4>, dim3((unsigned)a.units), dim3(256), lds, stream, pa, a,
                        pt_positions);
   else

@@ -162,8 +162,11 @@ __device__ __forceinline__ void build_lists(Evicted evicted, int n_iter, int per
   }
 }
 
-template <bool STREAM>
+// KP: keys per thread held in registers (n <= 256 KP); KP = 0 streams the keys
+// from memory in every pass (any n up to kMaxCapAny)
+template <int KP>
 __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
+  constexpr bool STREAM = KP == 0;
   __shared__ uint32_t hist[512];
   __shared__ uint64_t s_prefix;
   __shared__ int s_need;
@@ -177,14 +180,24 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
   // TOVA's weights (any slot of the unit when the rule does not read them)
   const float* last = a.rule == BM_RANK_TOVA ? a.lastw + (int64_t)u * a.cap : score;
   const int per = (a.n + 255) / 256;
-  constexpr int KP = STREAM ? 1 : kMaxPer;
+  constexpr int NK = STREAM ? 1 : KP;
 
-  uint64_t key[KP];
+  uint64_t key[NK];
   if constexpr (!STREAM) {
+    // every load issued before any is used (indices clamped into range)
+    float sv[KP], lv[KP];
+    int pv[KP];
 #pragma unroll
-    for (int i = 0; i < kMaxPer; ++i) {
+    for (int i = 0; i < KP; ++i) {
+      const int jc = min(tid + 256 * i, a.n - 1);
+      sv[i] = score[jc];
+      lv[i] = last[jc];
+      pv[i] = pos[jc];
+    }
+#pragma unroll
+    for (int i = 0; i < KP; ++i) {
       const int j = tid + 256 * i;
-      key[i] = (i < per && j < a.n) ? rank_key(a.rule, score[j], last[j], pos[j], a.curr_id) : ~0ull;
+      key[i] = (i < per && j < a.n) ? rank_key(a.rule, sv[i], lv[i], pv[i], a.curr_id) : ~0ull;
     }
   }
   // key of entry tid + 256 i (registers, or recomputed when streaming)
@@ -196,7 +209,7 @@ __global__ void __launch_bounds__(256) select_kernel(EvictArgs a) {
       return key[i];
     }
   };
-  const int n_iter = STREAM ? per : kMaxPer;
+  const int n_iter = STREAM ? per : KP;
   const uint64_t thr = radix_kth(key_of, n_iter, per, a.n, a.n - a.kv_max, position_bits(a.curr_id),
                                  hist, &s_prefix, &s_need);   // exactly n - kv_max keys are <= thr
 
@@ -432,9 +445,13 @@ hipError_t launch_fold_cut(const PrefillArgs& pa, const EvictArgs& a, int pt_pos
 
 hipError_t launch_select(const EvictArgs& a, hipStream_t stream) {
   if (a.n > kMaxCap)
-    hipLaunchKernelGGL(select_kernel<true>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(select_kernel<0>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+  else if (a.n <= 256 * 3)
+    hipLaunchKernelGGL(select_kernel<3>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+  else if (a.n <= 256 * 4)
+    hipLaunchKernelGGL(select_kernel<4>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
   else
-    hipLaunchKernelGGL(select_kernel<false>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(select_kernel<kMaxPer>, dim3((unsigned)a.units), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

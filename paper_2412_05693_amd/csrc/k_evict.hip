@@ -48,24 +48,29 @@ __device__ __forceinline__ int block_excl_count(bool flag, int* s_wave, int* tot
 // 64-lane scan of the 256 bins).  Keys are unique (they hold the position), so
 // exactly `need` keys are <= the result.  The low 32 bits of every key are the
 // entry's position, which is at most curr_id: the digits of that word at and
-// above bit pos_bits are zero in every key, so their passes are skipped (they
-// would keep the prefix and `need` as they are).  The two 256-bin histograms
-// alternate between the passes, so clearing the next one needs no barrier of
-// its own: two barriers per pass.
+// above bit pos_bits are zero in every key, so only the four digits of the high
+// word and the position digits below pos_bits get a pass (the others would keep
+// the prefix and `need` as they are).  The two 256-bin histograms alternate
+// between the passes, so clearing the next one needs no barrier of its own: two
+// barriers per pass.  When the bin that holds the need-th key holds exactly the
+// `need` keys still wanted, every key of that bin is among the smallest: the
+// select stops there and returns the bin's prefix with all lower bits set, which
+// has the same keys at or below it as the need-th key itself.
 template <typename KeyOf>
 __device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per, int n, int need,
                                               int pos_bits, uint32_t* hist, uint64_t* s_prefix,
                                               int* s_need) {
   const int tid = threadIdx.x;
+  const int n_pos = (pos_bits + 7) >> 3;   // position digits that can be nonzero
+  const int n_pass = 4 + n_pos;
   uint64_t prefix = 0;
   hist[tid] = 0;
   __syncthreads();
-  int q = 0;   // passes run so far
-  for (int pass = 0; pass < 8; ++pass) {
-    const int shift = 56 - 8 * pass;
-    if (shift < 32 && shift >= pos_bits) continue;   // uniform across the workgroup
-    const uint64_t himask = pass == 0 ? 0ull : (~0ull << (shift + 8));
-    uint32_t* h = hist + 256 * (q & 1);
+  // pass r: the digit at `shift`, histogram r & 1 (r counts only the passes run)
+  for (int r = 0; r < n_pass; ++r) {
+    const int shift = r < 4 ? 56 - 8 * r : 8 * (n_pass - 1 - r);
+    const uint64_t himask = r == 0 ? 0ull : (~0ull << (shift + 8));
+    uint32_t* h = hist + 256 * (r & 1);
 #pragma unroll
     for (int i = 0; i < n_iter; ++i) {
       const int j = tid + 256 * i;
@@ -74,7 +79,7 @@ __device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per,
         if ((kk & himask) == prefix) atomicAdd(&h[(kk >> shift) & 255u], 1u);
       }
     }
-    hist[256 * ((q + 1) & 1) + tid] = 0;   // the next pass's histogram
+    hist[256 * ((r + 1) & 1) + tid] = 0;   // the next pass's histogram
     __syncthreads();
     if (tid < 64) {
       const uint32_t h0 = h[4 * tid], h1 = h[4 * tid + 1], h2 = h[4 * tid + 2], h3 = h[4 * tid + 3];
@@ -90,8 +95,11 @@ __device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per,
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         if ((int)ex < need && need <= (int)(ex + hv[b])) {
-          *s_prefix = prefix | ((uint64_t)(4 * tid + b) << shift);
-          *s_need = need - (int)ex;
+          const int rest = need - (int)ex;
+          const bool whole = rest == (int)hv[b];   // the whole bin is wanted
+          *s_prefix = prefix | ((uint64_t)(4 * tid + b) << shift) |
+                      (whole ? (1ull << shift) - 1 : 0ull);
+          *s_need = whole ? 0 : rest;
         }
         ex += hv[b];
       }
@@ -99,7 +107,7 @@ __device__ __forceinline__ uint64_t radix_kth(KeyOf key_of, int n_iter, int per,
     __syncthreads();
     prefix = *s_prefix;
     need = *s_need;
-    ++q;
+    if (need == 0) break;   // uniform: every thread read the same value
   }
   return prefix;
 }

@@ -1,0 +1,131 @@
+"""GPU: the cut alone (Sec. 3.1; the ranking of Sec. 3.2) on crafted cache states.
+
+Scores, positions and K/V rows are written straight into the cache, the
+context is rebuilt on that state (bm_resume) and bm_evict_compact runs the
+select and the compaction.  The sum rule ranks by the stored float itself, so
+the oracle's float64 order is exactly the device's and kept sets must agree
+entry for entry, with no near-tie allowance.
+
+The score patterns put the decision in every digit of the 64-bit key: the
+evicted and the kept entries part in the first, second, third or fourth byte
+of the float; all scores equal (the positions decide); a few tied values with
+the cut inside a tie; uniform and log-spread values with exact zeros.
+Positions reach past 2^16, so three position digits can take part.  Cache
+sizes cover the four select instantiations (3, 4 and 16 keys per thread, and
+the streaming form above 4096 entries), with 1 to 1024 entries removed.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import pd as opd
+from paper_2412_05693_amd.batchmax import PDAttention
+
+pytestmark = pytest.mark.gpu
+
+HEAD_DIM = 64
+CURR_ID = 70_000
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _bits(lo, hi, size, rng):
+    """float32 values whose bit patterns are drawn from [lo, hi)."""
+    return rng.integers(lo, hi, size=size, dtype=np.uint64).astype(np.uint32).view(np.float32)
+
+
+def _scores(kind, n, e, rng):
+    """n float32 scores of which the e smallest (ties by position) are the cut."""
+    kept = n - e
+    if kind == "byte0":      # [1, 2) against [2, 8): top byte 0x3f against 0x40
+        ev, kp = rng.uniform(1, 2, e), rng.uniform(2, 8, kept)
+    elif kind == "byte1":    # 0x4000xxxx against 0x4020xxxx and up
+        ev, kp = _bits(0x40000000, 0x40010000, e, rng), _bits(0x40200000, 0x40800000, kept, rng)
+    elif kind == "byte2":    # 0x400000xx against 0x400080xx and up
+        ev, kp = _bits(0x40000000, 0x40000100, e, rng), _bits(0x40008000, 0x40010000, kept, rng)
+    elif kind == "byte3":    # last byte below 0x40 against at or above it (many float ties)
+        ev, kp = _bits(0x40000000, 0x40000040, e, rng), _bits(0x40000040, 0x40000100, kept, rng)
+    elif kind == "equal":    # one value: the positions alone decide
+        return np.full(n, 1.0, dtype=np.float32)
+    elif kind == "ties":     # zeros, then a tie group that the cut splits, then ones
+        z = e // 2
+        half = min(n - z, e - z + max(1, kept // 2))
+        out = np.concatenate([np.zeros(z), np.full(half, 0.5), np.ones(n - z - half)])
+        return rng.permutation(out).astype(np.float32)
+    elif kind == "uniform":  # [0, 1) with exact zeros
+        x = rng.uniform(0, 1, n)
+        x[rng.random(n) < 0.05] = 0.0
+        return x.astype(np.float32)
+    elif kind == "spread":   # many exponents
+        return np.exp(rng.uniform(-60, 20, n)).astype(np.float32)
+    else:
+        raise ValueError(kind)
+    return rng.permutation(np.concatenate([ev, kp])).astype(np.float32)
+
+
+PATTERNS = (("byte0", "byte1", "byte2", "byte3"), ("equal", "ties", "uniform", "spread"))
+
+
+@pytest.mark.parametrize("n,e", [(700, 188), (768, 256), (1000, 1), (1000, 999), (3000, 1024),
+                                 (4096, 512), (5000, 777)],
+                         ids=lambda x: str(x))
+@pytest.mark.parametrize("patterns", PATTERNS, ids=("bytes", "ties"))
+def test_cut_on_crafted_state(n, e, patterns):
+    _need_gpu()
+    b, hk = 2, 2
+    kv_max = n - e
+    pd = PDAttention(b=b, s=CURR_ID + 1, kv_max=kv_max, block=e, max_gen=0, n_heads=hk,
+                     n_kv_heads=hk, head_dim=HEAD_DIM, dtype="f32", device="cuda", init=False)
+    assert pd.cap == n
+    rng = np.random.default_rng(n * 7919 + e)
+    units = [(bi, h) for bi in range(b) for h in range(hk)]
+    state = {}
+    score = np.zeros((b, hk, n), np.float32)
+    pos = np.zeros((b, hk, n), np.int32)
+    k = rng.standard_normal((b, hk, n, HEAD_DIM)).astype(np.float32)
+    v = rng.standard_normal((b, hk, n, HEAD_DIM)).astype(np.float32)
+    for (bi, h), kind in zip(units, patterns):
+        p = np.sort(rng.choice(CURR_ID + 1, size=n, replace=False))
+        pos[bi, h] = rng.permutation(p)
+        score[bi, h] = _scores(kind, n, e, rng)
+        state[(bi, h)] = kind
+    pd.score.copy_(torch.from_numpy(score))
+    pd.pos.copy_(torch.from_numpy(pos))
+    pd.k.copy_(torch.from_numpy(k))
+    pd.v.copy_(torch.from_numpy(v))
+    pd.len.fill_(n)
+    pd.resume(n, CURR_ID + 1)
+    pd.set_rank_rule("sum")
+    print(f"[select] n={n} e={e} patterns={patterns}", flush=True)
+    pd.evict_compact(CURR_ID)
+    torch.cuda.synchronize()
+    assert pd.length == kv_max
+    g_len = pd.len.cpu().numpy()
+    g_pos = pd.pos.cpu().numpy()
+    g_score = pd.score.cpu().numpy()
+    g_k, g_v = pd.k.cpu().numpy(), pd.v.cpu().numpy()
+    for bi, h in units:
+        tag = f"unit {(bi, h)} {state[(bi, h)]}"
+        assert g_len[bi, h] == kv_max, tag
+        orc = opd.UnitOracle(head_dim=HEAD_DIM, group=1, kv_max=kv_max, sm_scale=1.0, rule="sum")
+        orc.pos = pos[bi, h].astype(np.int64)
+        orc.score = score[bi, h].astype(np.float64)
+        orc.k = np.zeros((n, HEAD_DIM))
+        orc.v = np.zeros((n, HEAD_DIM))
+        orc.last_w = np.zeros(n)
+        ev = orc.evict(CURR_ID, "prefill")
+        kept = g_pos[bi, h, :kv_max]
+        assert np.array_equal(np.sort(kept), ev.kept_pos), tag
+        # every kept entry carries its own score and K/V rows
+        slot_of = {int(p): j for j, p in enumerate(pos[bi, h])}
+        src = np.array([slot_of[int(p)] for p in kept])
+        assert np.array_equal(g_score[bi, h, :kv_max], score[bi, h, src]), tag
+        assert np.array_equal(g_k[bi, h, :kv_max], k[bi, h, src]), tag
+        assert np.array_equal(g_v[bi, h, :kv_max], v[bi, h, src]), tag
+        # survivors already below kv_max stay in their slots (only holes are filled)
+        stay = np.isin(pos[bi, h, :kv_max], kept)
+        assert np.array_equal(kept[stay], pos[bi, h, :kv_max][stay]), tag
+    pd.close()

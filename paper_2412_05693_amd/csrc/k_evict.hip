@@ -5,13 +5,14 @@
 // (curr_id + 1 - pos_j) in IEEE float32 division) packed with its position into
 // one 64-bit integer (rank_key): the integer order is (key ascending, pos
 // ascending), so the smallest key goes first and, on an exact tie, the older
-// entry (the tie rule of the oracle).  An 8-pass LDS radix select over 8-bit
-// digits finds the E-th smallest key exactly (positions are unique, so exactly
-// E keys are <= it).  Up to kMaxCap keys stay in registers; larger caches
-// recompute each key from the scores and positions in every pass.  Evicted slots below kv_max become
-// holes, surviving slots at or above kv_max become sources; both lists are
-// built in slot order with a workgroup prefix count, so the pairing is
-// deterministic.
+// entry.  An LDS radix select over 8-bit digits (at most 8 passes, fewer when
+// curr_id needs fewer position digits or a pass already settles the cut) finds
+// a threshold with exactly E keys at or below it (positions are unique, so the
+// E smallest keys are well defined).  Up to kMaxCap keys stay in registers;
+// larger caches recompute each key from the scores and positions in every
+// pass.  Evicted slots below kv_max become holes, surviving slots at or above
+// kv_max become sources; both lists are built in slot order with workgroup
+// prefix counts, so the pairing is deterministic.
 //
 // K3 (compact_kernel), units x chunks of 32 moves: the i-th source moves into
 // the i-th hole (K row, V row, score, pos), 16-byte coalesced copies.  Sources

@@ -819,8 +819,10 @@ __global__ void __launch_bounds__(kThreads, (BF16 || D == 64) ? 2 : 1) prefill_a
 // Fold the per-workgroup partial column sums into the scores, in workgroup
 // order: score[j] = (j < len0 ? score[j] : 0) + sum over workgroups that saw j
 // (without accumulation: new entries get 0, older scores stay).
-// Grid: (units, slot chunks of 256); every thread owns one slot and issues its
-// partial-sum loads together.
+// Grid: (units, slot chunks of 256); every thread owns one slot.  The partial
+// rows are read eight at a time, all eight loads issued before any is used:
+// row indices are clamped into the rows the slot has and the terms outside
+// them are selected to zero, so the sum keeps its order bit for bit.
 __global__ void __launch_bounds__(256) score_reduce_kernel(PrefillArgs a, int pt_positions) {
   const int u = blockIdx.x;
   const int n = a.len0 + a.n_tok;
@@ -829,10 +831,19 @@ __global__ void __launch_bounds__(256) score_reduce_kernel(PrefillArgs a, int pt
     const float* part = a.partial + (int64_t)u * a.npt_stride * a.cap + j;
     float* score = a.score + (int64_t)u * a.cap;
     const int pt0 = j < a.len0 ? 0 : (j - a.len0) / pt_positions;
+    const int last = a.npt_used - 1;
     float acc = j < a.len0 ? score[j] : 0.0f;
     if (a.accumulate) {
-#pragma unroll 8
-      for (int pt = pt0; pt < a.npt_used; ++pt) acc += part[(int64_t)pt * a.cap];
+      for (int c0 = pt0 & ~7; c0 <= last; c0 += 8) {
+        float x[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) x[c] = part[(int64_t)min(max(c0 + c, pt0), last) * a.cap];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const int pt = c0 + c;
+          acc += pt >= pt0 && pt <= last ? x[c] : 0.0f;
+        }
+      }
     }
     score[j] = acc;
   }

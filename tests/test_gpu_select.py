@@ -13,6 +13,8 @@ the cut inside a tie; uniform and log-spread values with exact zeros.
 Positions reach past 2^16, so three position digits can take part.  Cache
 sizes cover the four select instantiations (3, 4 and 16 keys per thread, and
 the streaming form above 4096 entries), with 1 to 1024 entries removed.
+The paper's own rule (the average) is checked the same way on scores built so
+that every quotient is exact.
 """
 import numpy as np
 import pytest
@@ -69,11 +71,9 @@ def _scores(kind, n, e, rng):
 PATTERNS = (("byte0", "byte1", "byte2", "byte3"), ("equal", "ties", "uniform", "spread"))
 
 
-@pytest.mark.parametrize("n,e", [(700, 188), (768, 256), (1000, 1), (1000, 999), (3000, 1024),
-                                 (4096, 512), (5000, 777)],
-                         ids=lambda x: str(x))
-@pytest.mark.parametrize("patterns", PATTERNS, ids=("bytes", "ties"))
-def test_cut_on_crafted_state(n, e, patterns):
+def _run_cut(n, e, rule, make_unit, tags):
+    """Write a crafted state into a 2 x 2-unit cache, cut it, compare with the oracle.
+    make_unit(rng, unit_index) -> (positions, float32 scores) of the unit's n entries."""
     _need_gpu()
     b, hk = 2, 2
     kv_max = n - e
@@ -82,24 +82,20 @@ def test_cut_on_crafted_state(n, e, patterns):
     assert pd.cap == n
     rng = np.random.default_rng(n * 7919 + e)
     units = [(bi, h) for bi in range(b) for h in range(hk)]
-    state = {}
     score = np.zeros((b, hk, n), np.float32)
     pos = np.zeros((b, hk, n), np.int32)
     k = rng.standard_normal((b, hk, n, HEAD_DIM)).astype(np.float32)
     v = rng.standard_normal((b, hk, n, HEAD_DIM)).astype(np.float32)
-    for (bi, h), kind in zip(units, patterns):
-        p = np.sort(rng.choice(CURR_ID + 1, size=n, replace=False))
-        pos[bi, h] = rng.permutation(p)
-        score[bi, h] = _scores(kind, n, e, rng)
-        state[(bi, h)] = kind
+    for i, (bi, h) in enumerate(units):
+        pos[bi, h], score[bi, h] = make_unit(rng, i)
     pd.score.copy_(torch.from_numpy(score))
     pd.pos.copy_(torch.from_numpy(pos))
     pd.k.copy_(torch.from_numpy(k))
     pd.v.copy_(torch.from_numpy(v))
     pd.len.fill_(n)
     pd.resume(n, CURR_ID + 1)
-    pd.set_rank_rule("sum")
-    print(f"[select] n={n} e={e} patterns={patterns}", flush=True)
+    pd.set_rank_rule(rule)
+    print(f"[select] n={n} e={e} rule={rule} patterns={tags}", flush=True)
     pd.evict_compact(CURR_ID)
     torch.cuda.synchronize()
     assert pd.length == kv_max
@@ -107,10 +103,10 @@ def test_cut_on_crafted_state(n, e, patterns):
     g_pos = pd.pos.cpu().numpy()
     g_score = pd.score.cpu().numpy()
     g_k, g_v = pd.k.cpu().numpy(), pd.v.cpu().numpy()
-    for bi, h in units:
-        tag = f"unit {(bi, h)} {state[(bi, h)]}"
+    for i, (bi, h) in enumerate(units):
+        tag = f"unit {(bi, h)} {tags[i]}"
         assert g_len[bi, h] == kv_max, tag
-        orc = opd.UnitOracle(head_dim=HEAD_DIM, group=1, kv_max=kv_max, sm_scale=1.0, rule="sum")
+        orc = opd.UnitOracle(head_dim=HEAD_DIM, group=1, kv_max=kv_max, sm_scale=1.0, rule=rule)
         orc.pos = pos[bi, h].astype(np.int64)
         orc.score = score[bi, h].astype(np.float64)
         orc.k = np.zeros((n, HEAD_DIM))
@@ -129,3 +125,49 @@ def test_cut_on_crafted_state(n, e, patterns):
         stay = np.isin(pos[bi, h, :kv_max], kept)
         assert np.array_equal(kept[stay], pos[bi, h, :kv_max][stay]), tag
     pd.close()
+
+
+def _positions(rng, n):
+    return rng.permutation(np.sort(rng.choice(CURR_ID + 1, size=n, replace=False))).astype(np.int32)
+
+
+SIZES = [(700, 188), (768, 256), (1000, 1), (1000, 999), (3000, 1024), (4096, 512), (5000, 777)]
+
+
+@pytest.mark.parametrize("n,e", SIZES, ids=lambda x: str(x))
+@pytest.mark.parametrize("patterns", PATTERNS, ids=("bytes", "ties"))
+def test_cut_on_crafted_state(n, e, patterns):
+    def unit(rng, i):
+        return _positions(rng, n), _scores(patterns[i], n, e, rng)
+
+    _run_cut(n, e, "sum", unit, patterns)
+
+
+AVE_PATTERNS = ("equal", "ties", "dyadic", "dyadic_small")
+
+
+@pytest.mark.parametrize("n,e", SIZES, ids=lambda x: str(x))
+def test_cut_ave_rule_exact_quotients(n, e):
+    """The paper's rule (Sec. 3.2: sum_weights / (curr_id + 1 - kv_ids)) with
+    scores built as target x (curr_id + 1 - pos) exactly, for targets with few
+    mantissa bits: the quotient is the target itself in any correctly rounded
+    float32 division, so the device's keys equal the oracle's float64 averages
+    and the kept sets must match exactly (many exact ties: positions decide)."""
+    def unit(rng, i):
+        p = _positions(rng, n)
+        kind = AVE_PATTERNS[i]
+        if kind == "equal":
+            t = np.full(n, 0.25)
+        elif kind == "ties":
+            t = rng.choice([0.0, 0.125, 0.5], size=n)
+        elif kind == "dyadic":
+            t = rng.integers(0, 64, size=n) / 64.0
+        else:
+            t = rng.integers(1, 64, size=n) * 2.0 ** -30
+        den = (CURR_ID + 1 - p.astype(np.int64)).astype(np.float64)
+        sc = (t * den).astype(np.float32)
+        assert np.array_equal(sc.astype(np.float64), t * den)          # exact products
+        assert np.array_equal(sc.astype(np.float64) / den, t)           # exact quotients
+        return p, sc
+
+    _run_cut(n, e, "ave", unit, AVE_PATTERNS)

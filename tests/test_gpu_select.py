@@ -171,3 +171,64 @@ def test_cut_ave_rule_exact_quotients(n, e):
         return p, sc
 
     _run_cut(n, e, "ave", unit, AVE_PATTERNS)
+
+
+@pytest.mark.parametrize("kv_max", [511, 1023, 4095])
+def test_decode_eviction_exact_ties(kv_max):
+    """One decode step (append, attend, one eviction; Algorithm 1's decoding
+    loop, one removal per step) on a crafted full cache.  A zero query gives
+    every one of the kv_max + 1 entries the weight 1 / (kv_max + 1), a power of
+    two, so the updated scores (multiples of 2^-12 below 2) are exact on both
+    sides; under the sum rule the smallest score is held by many entries (the
+    cached ones that had none, and the new one) and the oldest of them must go.
+    Scores, kept sets and outputs against the oracle."""
+    _need_gpu()
+    b, hk, G = 2, 2, 2
+    H, p = hk * G, CURR_ID + 1
+    pd = PDAttention(b=b, s=p, kv_max=kv_max, block=256, max_gen=1, n_heads=H, n_kv_heads=hk,
+                     head_dim=HEAD_DIM, dtype="f32", device="cuda", init=False)
+    rng = np.random.default_rng(kv_max)
+    cap = pd.cap
+    score = np.zeros((b, hk, cap), np.float32)
+    pos = np.zeros((b, hk, cap), np.int32)
+    k = rng.standard_normal((b, hk, cap, HEAD_DIM)).astype(np.float32)
+    v = rng.standard_normal((b, hk, cap, HEAD_DIM)).astype(np.float32)
+    for bi in range(b):
+        for h in range(hk):
+            pos[bi, h, :kv_max] = _positions(rng, kv_max)
+            # zero scores tie, after the update, with the new entry's own weight
+            score[bi, h, :kv_max] = rng.choice([0, 3, 5, 900], size=kv_max) * 2.0 ** -12
+    q = torch.zeros((b, H, 1, HEAD_DIM), dtype=torch.float32, device="cuda")
+    kn = rng.standard_normal((b, hk, 1, HEAD_DIM)).astype(np.float32)
+    vn = rng.standard_normal((b, hk, 1, HEAD_DIM)).astype(np.float32)
+    o = torch.zeros_like(q)
+    for dst, src in ((pd.score, score), (pd.pos, pos), (pd.k, k), (pd.v, v)):
+        dst.copy_(torch.from_numpy(src))
+    pd.len.fill_(kv_max)
+    pd.resume(kv_max, p)
+    pd.set_rank_rule("sum")
+    print(f"[select] decode step kv_max={kv_max}", flush=True)
+    pd.decode_step(p, q, torch.from_numpy(kn).cuda(), torch.from_numpy(vn).cuda(), o, row=0)
+    torch.cuda.synchronize()
+    assert pd.length == kv_max
+    g_pos, g_score = pd.pos.cpu().numpy(), pd.score.cpu().numpy()
+    g_o = o.cpu().numpy()
+    for bi in range(b):
+        for h in range(hk):
+            tag = f"unit {(bi, h)}"
+            orc = opd.UnitOracle(head_dim=HEAD_DIM, group=G, kv_max=kv_max, sm_scale=1.0,
+                                 rule="sum")
+            orc.pos = pos[bi, h, :kv_max].astype(np.int64)
+            orc.score = score[bi, h, :kv_max].astype(np.float64)
+            orc.k = k[bi, h, :kv_max].astype(np.float64)
+            orc.v = v[bi, h, :kv_max].astype(np.float64)
+            orc.last_w = np.zeros(kv_max)
+            ref, ev = orc.decode_step(p, np.zeros((G, HEAD_DIM)), kn[bi, h, 0], vn[bi, h, 0])
+            assert ev is not None and ev.gap == 0.0, tag      # the cut falls inside a tie
+            kept = g_pos[bi, h, :kv_max]
+            assert np.array_equal(np.sort(kept), ev.kept_pos), tag
+            by_pos = dict(zip(orc.pos.tolist(), orc.score.tolist()))
+            assert all(float(g_score[bi, h, j]) == by_pos[int(kept[j])] for j in range(kv_max)), tag
+            err = np.max(np.abs(g_o[bi, h * G:(h + 1) * G, 0] - ref))
+            assert err <= 1e-4, (tag, err)
+    pd.close()
